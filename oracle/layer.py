@@ -1,0 +1,89 @@
+"""Oracle: the attention block around the kernel -- projections in, out.
+
+TEST INFRASTRUCTURE ONLY (see ``oracle/__init__.py``).
+
+The block follows the paper's description of one device's attention stage
+(Section 3.2 walk-through of DS-Ulysses, Section 3.3 and the Appendix A
+paragraphs "Untied Ulysses (forward)" / "(backward)"): the hidden states X
+are projected to Q, K, V, attention runs per head, the per-head outputs fill
+``final_out`` and the output projection proj_o maps it back to d_model.
+
+Weight layout used here (no bias, no rotary embedding, no normalisation):
+    x    [S, dm]
+    wqkv [dm, (Hq + 2 Hkv) d]  columns = [Q heads | K heads | V heads],
+                               each head a block of d consecutive columns
+    wo   [Hq d, dm]            rows = the heads of final_out, in order
+    y    [S, dm] = final_out.reshape(S, Hq d) @ wo
+
+Backward (chain rule on the same definition):
+    dO    = dY wo^T              dWo   = final_out^T dY
+    dQ, dK, dV from the attention gradient
+    dX    = [dQ|dK|dV] wqkv^T    dWqkv = X^T [dQ|dK|dV]
+"""
+
+import numpy as np
+
+from . import attention
+
+
+def split_qkv(qkv, Hq, Hkv, d):
+    S = qkv.shape[0]
+    q = qkv[:, :Hq * d].reshape(S, Hq, d)
+    k = qkv[:, Hq * d:(Hq + Hkv) * d].reshape(S, Hkv, d)
+    v = qkv[:, (Hq + Hkv) * d:].reshape(S, Hkv, d)
+    return q, k, v
+
+
+def layer_fwd(x, wqkv, wo, Hq, Hkv, d, causal=True):
+    """Returns (y [S, dm], final_out [S, Hq, d], lse [Hq, S])."""
+    x = np.asarray(x, np.float64)
+    wqkv = np.asarray(wqkv, np.float64)
+    wo = np.asarray(wo, np.float64)
+    S = x.shape[0]
+    q, k, v = split_qkv(x @ wqkv, Hq, Hkv, d)
+    o, lse = attention.attn_fwd(q, k, v, causal)
+    y = o.reshape(S, Hq * d) @ wo
+    return y, o, lse
+
+
+def layer_bwd(x, wqkv, wo, dy, Hq, Hkv, d, causal=True):
+    """Returns (dx [S, dm], dwqkv [dm, (Hq+2Hkv)d], dwo [Hq d, dm])."""
+    x = np.asarray(x, np.float64)
+    wqkv = np.asarray(wqkv, np.float64)
+    wo = np.asarray(wo, np.float64)
+    dy = np.asarray(dy, np.float64)
+    S = x.shape[0]
+    q, k, v = split_qkv(x @ wqkv, Hq, Hkv, d)
+    o, _ = attention.attn_fwd(q, k, v, causal)
+    do = (dy @ wo.T).reshape(S, Hq, d)
+    dwo = o.reshape(S, Hq * d).T @ dy
+    dq, dk, dv = attention.attn_bwd(q, k, v, do, causal)
+    dqkv = np.concatenate([dq.reshape(S, -1), dk.reshape(S, -1),
+                           dv.reshape(S, -1)], axis=1)
+    dx = dqkv @ wqkv.T
+    dwqkv = x.T @ dqkv
+    return dx, dwqkv, dwo
+
+
+def layer_fwd_rows(x, wqkv, wo, Hq, Hkv, d, rows):
+    """y, final_out and lse at the listed rows only (causal).
+
+    K and V are needed for every position (each row sees all earlier keys),
+    Q and the output only at the listed rows.
+    """
+    x = np.asarray(x, np.float64)
+    wqkv = np.asarray(wqkv, np.float64)
+    wo = np.asarray(wo, np.float64)
+    rows = np.asarray(rows, np.int64)
+    S = x.shape[0]
+    kv = x @ wqkv[:, Hq * d:]
+    k = kv[:, :Hkv * d].reshape(S, Hkv, d)
+    v = kv[:, Hkv * d:].reshape(S, Hkv, d)
+    qr = (x[rows] @ wqkv[:, :Hq * d]).reshape(len(rows), Hq, d)
+    # Place the sampled query rows at their own positions; other rows are
+    # never read because each listed row only sees keys <= itself.
+    q = np.zeros((S, Hq, d))
+    q[rows] = qr
+    o, lse = attention.attn_fwd(q, k, v, True, rows=rows)
+    y = o.reshape(len(rows), Hq * d) @ wo
+    return y, o, lse
