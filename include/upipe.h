@@ -1,0 +1,200 @@
+/*
+ * upipe.h -- C ABI of the MI355X (gfx950) head-chunked causal GQA attention
+ * library: the per-GPU hot path of UPipe ("Untied Ulysses", arXiv 2602.21196).
+ *
+ * After the Ulysses re-layout (paper Section 3.1) one GPU holds the full
+ * sequence S for its share of heads: Hq query heads and Hkv key/value heads,
+ * head width d.  UPipe (Section 3.3) runs the attention block over those heads
+ * in nu = Hq/U chunks of U heads, reusing one chunk-sized set of buffers for
+ * every chunk, so activation scratch grows with U rather than with Hq.  Query
+ * head h reads key/value head h / (Hq/Hkv) (grouped-query attention, Section
+ * 2.1; chunks follow the GQA schedule of Section 4.1, which on one device is
+ * ascending local head order).
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Element types: bf16 tensors are raw IEEE bfloat16 (2 bytes), fp32 is
+ *    IEEE binary32.  All tensors are dense, contiguous, row-major, with the
+ *    shapes stated per call, and 16-byte aligned.
+ *  - Pointers: all tensor and workspace pointers are DEVICE pointers owned by
+ *    the caller.  The library never allocates, frees or synchronises device
+ *    memory in the compute entry points; every kernel is enqueued on the
+ *    caller's `stream`, and the calls return as soon as the work is queued.
+ *  - Workspace: each compute call takes a caller-allocated device workspace of
+ *    at least the size returned by its *_workspace_size query.  It holds the
+ *    chunk-sized buffers that are reused for every chunk plus the buffers
+ *    that live for the whole call; its contents on entry are ignored.
+ *  - Outputs are overwritten, never accumulated into.
+ *  - Scale: scores are q.k / sqrt(d) (Section 2.1); there is no scale knob.
+ *  - Causal: key j is visible to query i iff j <= i.  causal = 0 gives full
+ *    (bidirectional) attention over all S keys.
+ *  - Determinism: for fixed shapes every output is bitwise identical across
+ *    calls and across every valid U (one fixed reduction order: query heads
+ *    ascending, then query blocks ascending; fp32 partial sums are carried
+ *    between chunks through the workspace).
+ *  - Errors: arguments are validated on the host before anything is
+ *    enqueued; a failing call enqueues nothing and returns a negative
+ *    upipe_status.  A launch failure returns UPIPE_ERR_HIP (work queued
+ *    before it stays queued).  Faults inside kernels surface at the caller's
+ *    next synchronisation.  No C++ exception crosses this interface.
+ *  - Supported shapes: d == 128; S >= 1 (any length: rows past the last tile
+ *    are padded inside the workspace); 1 <= Hkv <= Hq, Hkv | Hq; 1 <= U,
+ *    U | Hq; Hq <= 64; S * max(Hq, d_model/128) * d < 2^40.
+ *  - Thread safety: calls are reentrant across host threads and streams as
+ *    long as each concurrent call has its own workspace and outputs.  The
+ *    profiling switch below is process-global and not thread-safe.
+ */
+#ifndef UPIPE_H
+#define UPIPE_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  UPIPE_OK = 0,
+  UPIPE_ERR_INVALID_ARG = -1, /* bad size, null/misaligned pointer, U or Hkv
+                                 not dividing Hq, workspace too small      */
+  UPIPE_ERR_UNSUPPORTED = -2, /* valid in principle, not built: d != 128,
+                                 d_model % 128 != 0, Hq > 64, too large     */
+  UPIPE_ERR_WORKSPACE = -3,   /* ws_bytes below the size query's result     */
+  UPIPE_ERR_HIP = -4          /* a HIP runtime call or launch failed        */
+} upipe_status;
+
+/* Human-readable name of a status code (static storage, never NULL). */
+const char* upipe_status_string(int status);
+
+/* Library ABI version: major*10000 + minor*100 + patch. */
+int upipe_version(void);
+
+/* ------------------------------------------------------------------------
+ * Head schedule (paper Section 4.1 "Grouped-Query Attention Scheduling",
+ * Section 3.3 stage count nu = H/U).  Pure host computation.
+ *
+ * Global view with H query heads, Hkv key/value heads, C devices and U heads
+ * per stage (U a multiple of C, C | H, C | Hkv, U | H).  Device p owns query
+ * heads [p H/C, (p+1) H/C) and key/value heads [p Hkv/C, (p+1) Hkv/C).
+ * Stage s processes, on every device, the next U/C of its heads in ascending
+ * order, so a key/value head is sent only at the first stage that reads it.
+ *
+ *   stage_heads: host array of H ints; on return stage_heads[s*U + j] is the
+ *                j-th global query head of stage s, listed device by device.
+ *   kv_stage:    host array of Hkv ints; kv_stage[g] is the stage at which
+ *                key/value head g is first sent.
+ * Returns UPIPE_OK or UPIPE_ERR_INVALID_ARG (nothing written then).
+ * ---------------------------------------------------------------------- */
+int upipe_gqa_schedule(int H, int Hkv, int C, int U, int* stage_heads,
+                       int* kv_stage);
+
+/* ------------------------------------------------------------------------
+ * Workspace size queries.  Return the byte count the matching compute call
+ * needs for these shapes, or 0 if the shapes are invalid or unsupported.
+ * The size is  fixed(S, Hkv[, d_model]) + U * per_head(S)  (chunk buffers).
+ * ---------------------------------------------------------------------- */
+size_t upipe_attn_fwd_workspace_size(int64_t S, int Hq, int Hkv, int d, int U);
+size_t upipe_attn_bwd_workspace_size(int64_t S, int Hq, int Hkv, int d, int U);
+size_t upipe_layer_fwd_workspace_size(int64_t S, int d_model, int Hq, int Hkv,
+                                      int d, int U);
+size_t upipe_layer_bwd_workspace_size(int64_t S, int d_model, int Hq, int Hkv,
+                                      int d, int U);
+
+/* ------------------------------------------------------------------------
+ * Attention forward, head chunk by head chunk (Section 2.1 definition,
+ * Section 3.3 chunking, Appendix A "Untied Ulysses (forward)").
+ *
+ *   q   bf16 [S, Hq, d]   queries, token-major (the Ulysses layout)
+ *   k   bf16 [S, Hkv, d]  keys
+ *   v   bf16 [S, Hkv, d]  values
+ *   o   bf16 [S, Hq, d]   out: softmax(q k^T / sqrt d) v per head
+ *   lse fp32 [Hq, S]      out: natural-log log-sum-exp of each row's scaled
+ *                         scores (saved for the backward)
+ * For each chunk c the U heads [cU, (c+1)U) are packed to a head-major chunk
+ * buffer (the stand-in for the input all-to-all's destination), attended, and
+ * unpacked into o (the output all-to-all's target, `final_out`).
+ * ---------------------------------------------------------------------- */
+int upipe_attn_fwd(const void* q, const void* k, const void* v, void* o,
+                   float* lse, int64_t S, int Hq, int Hkv, int d, int causal,
+                   int U, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Attention backward (analytic gradient of the Section 2.1 definition,
+ * Appendix A "Untied Ulysses (backward)": per-stage dQ, per-group dK/dV
+ * accumulators that persist across stages).
+ *
+ *   q, k, v, o, lse  as produced/consumed by upipe_attn_fwd
+ *   dout bf16 [S, Hq, d]   upstream gradient of o
+ *   dq   bf16 [S, Hq, d]   out
+ *   dk   bf16 [S, Hkv, d]  out: summed over each group's query heads
+ *   dv   bf16 [S, Hkv, d]  out
+ * `lse` must come from upipe_attn_fwd on the same q, k, v (it is used to
+ * rebuild the probabilities without a second softmax pass).
+ * ---------------------------------------------------------------------- */
+int upipe_attn_bwd(const void* q, const void* k, const void* v, const void* o,
+                   const float* lse, const void* dout, void* dq, void* dk,
+                   void* dv, int64_t S, int Hq, int Hkv, int d, int causal,
+                   int U, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Attention block forward (Section 3.3: per stage, QKV projection of the
+ * stage's heads, attention, output written into `final_out`; the output
+ * projection is accumulated per chunk in fp32).  Always causal.
+ *
+ *   x         bf16 [S, d_model]                  hidden states
+ *   wqkv      bf16 [d_model, (Hq + 2 Hkv) d]     columns [Q heads|K|V]
+ *   wo        bf16 [Hq d, d_model]               output projection
+ *   y         bf16 [S, d_model]                  out: final_out @ wo
+ *   o_saved   bf16 [S, Hq, d]                    out: final_out (attention
+ *                                                output, saved for backward)
+ *   lse_saved fp32 [Hq, S]                       out: row log-sum-exp
+ * d_model must be a multiple of 128.
+ * ---------------------------------------------------------------------- */
+int upipe_layer_fwd(const void* x, const void* wqkv, const void* wo, void* y,
+                    void* o_saved, float* lse_saved, int64_t S, int d_model,
+                    int Hq, int Hkv, int d, int U, void* ws, size_t ws_bytes,
+                    hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Attention block backward (Appendix A "Untied Ulysses (backward)"): per
+ * chunk, dO = dY wo_c^T, dWo_c = O_c^T dY, Q_c recomputed from x, attention
+ * backward, dX += dQ_c wq_c^T, dWq_c = x^T dQ_c; after the last chunk
+ * dX += dK wk^T + dV wv^T, dWk = x^T dK, dWv = x^T dV.  K and V are
+ * recomputed from x (activation checkpointing keeps only x, final_out, lse).
+ *
+ *   x, wqkv, wo        as for upipe_layer_fwd
+ *   o_saved, lse_saved the forward's outputs for the same x and weights
+ *   dy    bf16 [S, d_model]                 upstream gradient of y
+ *   dx    bf16 [S, d_model]                 out
+ *   dwqkv bf16 [d_model, (Hq + 2 Hkv) d]    out
+ *   dwo   bf16 [Hq d, d_model]              out
+ * Weight gradients reduce over S with a fixed split of the sequence and a
+ * fixed-order sum of the partial products (deterministic, no atomics).
+ * ---------------------------------------------------------------------- */
+int upipe_layer_bwd(const void* x, const void* wqkv, const void* wo,
+                    const void* o_saved, const float* lse_saved,
+                    const void* dy, void* dx, void* dwqkv, void* dwo,
+                    int64_t S, int d_model, int Hq, int Hkv, int d, int U,
+                    void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Kernel timing (measurement aid).  While enabled, every kernel the library
+ * launches is bracketed by two HIP events recorded on the launch stream.
+ * upipe_profile_query() waits for the recorded events and reports, for the
+ * kernel family `name` (see upipe_profile_name), the number of launches and
+ * their summed duration in milliseconds since the last reset.  Enabling
+ * creates events with hipEventCreate; the switch is process-global.
+ * ---------------------------------------------------------------------- */
+int upipe_profile_enable(int on);
+int upipe_profile_reset(void);
+int upipe_profile_query(const char* name, int* launches, double* total_ms);
+/* Name of kernel family i (0 <= i < count), or NULL past the end. */
+const char* upipe_profile_name(int i);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* UPIPE_H */

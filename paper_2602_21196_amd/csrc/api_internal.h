@@ -1,0 +1,81 @@
+// Host-only internals shared by the ABI translation units.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "common.h"
+
+namespace upipe {
+
+constexpr int kMaxHeads = 64;
+constexpr int64_t kMaxSeq = int64_t(1) << 30;
+
+// Kernel families for event timing; order matches kFamilyNames in api.cpp.
+enum Family {
+  kPackRows = 0,
+  kUnpackRows,
+  kRowdotLse,
+  kAttnFwd,
+  kAttnBwdDkdv,
+  kAttnBwdDq,
+  kGemm,
+  kGemmWgrad,
+  kReduceSplitk,
+  kTransposeW,
+  kCastF32,
+};
+
+// Records HIP events around one launch when profiling is on.
+class ProfScope {
+ public:
+  ProfScope(int family, hipStream_t st);
+  ~ProfScope();
+
+ private:
+  hipStream_t st_;
+  hipEvent_t start_ = nullptr, stop_ = nullptr;
+  int family_ = -1;
+};
+
+#define UPIPE_LAUNCH(family, stream, expr)           \
+  do {                                               \
+    ::upipe::ProfScope _ps((family), (stream));      \
+    if ((expr) != hipSuccess) return UPIPE_ERR_HIP;  \
+  } while (0)
+
+bool aligned16(const void* p);
+int check_attn_shape(int64_t S, int Hq, int Hkv, int d, int U);
+bool group_split(int Hq, int Hkv, int U);
+
+// Bump allocator over the caller's workspace (256-byte aligned offsets).
+struct Carver {
+  size_t used = 0;
+  size_t take(size_t bytes);
+};
+
+struct AttnFwdPlan {
+  int64_t Sp = 0;
+  size_t Kp = 0, Vt = 0, Qc = 0, Oc = 0, total = 0;
+};
+
+struct AttnBwdPlan {
+  int64_t Sp = 0;
+  bool carry = false;  // a key/value group spans several chunks
+  size_t Kp = 0, Kt = 0, Vp = 0, dK32 = 0, dV32 = 0;
+  size_t Qc = 0, Qct = 0, dOc = 0, dOct = 0, dQc = 0, D = 0, lse_c = 0;
+  size_t total = 0;
+};
+
+AttnFwdPlan plan_attn_fwd(int64_t S, int Hq, int Hkv, int U);
+AttnBwdPlan plan_attn_bwd(int64_t S, int Hq, int Hkv, int U);
+
+int run_attn_fwd(const bf16* q, const bf16* k, const bf16* v, bf16* o,
+                 float* lse, int64_t S, int Hq, int Hkv, int causal, int U,
+                 char* ws, hipStream_t st);
+int run_attn_bwd(const bf16* q, const bf16* k, const bf16* v, const bf16* o,
+                 const float* lse, const bf16* dout, bf16* dq, bf16* dk,
+                 bf16* dv, int64_t S, int Hq, int Hkv, int causal, int U,
+                 char* ws, hipStream_t st);
+
+}  // namespace upipe

@@ -1,0 +1,59 @@
+// Shared device-side helpers for the gfx950 kernels.
+//
+// MFMA fragment conventions used throughout (v_mfma_f32_32x32x16_bf16, wave64):
+//   A operand: lane l supplies row (l % 32) of the 32x16 A tile and the 8
+//              k-values of k-group g = l / 32.
+//   B operand: lane l supplies column (l % 32) of the 16x32 B tile and the 8
+//              k-values of k-group g.
+//   The k-values a lane supplies may be any fixed permutation of the 16 k's
+//   as long as A and B use the same one; contractions only need agreement.
+//   C/D:       lane l holds column (l % 32); element i of its 16 floats is
+//              row 8*(i/4) + 4*g + (i%4).
+//
+// "MFMA order" of a transposed copy: a buffer stored [d][S] (sequence index
+// contiguous) keeps, inside every aligned block of 16 positions, the element
+// of sequence index perm16(p) at position p, where perm16 swaps bits 2 and 3.
+// Then the 16 floats one lane holds in a C tile (rows 8a+4g+b) become, after
+// conversion to bf16, exactly the B/A-operand vectors that read 8 consecutive
+// positions 16*kt + 8*g + j of such a buffer.  perm16 is an involution.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace upipe {
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int HEAD_DIM = 128;   // the only supported head width
+constexpr int SEQ_PAD = 128;    // sequence padding granule of packed buffers
+
+__host__ __device__ inline int64_t perm16(int64_t p) {
+  return (p & ~int64_t(12)) | ((p & 4) << 1) | ((p & 8) >> 1);
+}
+
+__host__ __device__ inline int64_t round_up(int64_t x, int64_t m) {
+  return (x + m - 1) / m * m;
+}
+
+__device__ __forceinline__ f32x16 mfma32x32x16(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ float fast_exp2(float x) {
+  return __builtin_amdgcn_exp2f(x);
+}
+
+__device__ __forceinline__ bf16x8 lds_read_b128(const char* base, uint32_t off) {
+  return *reinterpret_cast<const bf16x8*>(base + off);
+}
+
+__device__ __forceinline__ void lds_write_b128(char* base, uint32_t off, u32x4 v) {
+  *reinterpret_cast<u32x4*>(base + off) = v;
+}
+
+}  // namespace upipe

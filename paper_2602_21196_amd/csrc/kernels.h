@@ -1,0 +1,55 @@
+// Host-side launchers of the gfx950 kernels.  Every launcher enqueues on the
+// given stream and returns the launch status; shapes are validated by the
+// caller (api.cpp) before any of these run.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "common.h"
+
+namespace upipe {
+
+// ---- layout (layout.hip) -------------------------------------------------
+// src [S, H, d] heads h0..h0+n-1  ->  dst [n, Sp, d] and/or dst_t [n, d, Sp]
+// (MFMA order); rows >= S are zero.  Either destination may be null.
+hipError_t launch_pack_rows(const bf16* src, int64_t S, int H, int h0, int n,
+                            int64_t Sp, bf16* dst, bf16* dst_t, hipStream_t st);
+// src [n, Sp, d] rows < S  ->  dst [S, H, d] heads h0..h0+n-1.
+hipError_t launch_unpack_rows(const bf16* src, int64_t S, int H, int h0, int n,
+                              int64_t Sp, bf16* dst, hipStream_t st);
+// D[n, Sp] = rowsum(a * b) over the head width and lse_c[n, Sp] = the lse
+// rows h0.. of the caller's [Hq, S] array (both zero for rows >= S).  Element
+// (s, hh, e) of a is a[s * a_row + hh * a_head + e], likewise for b.
+hipError_t launch_rowdot_lse(const bf16* a, int64_t a_row, int64_t a_head,
+                             const bf16* b, int64_t b_row, int64_t b_head,
+                             const float* lse, int64_t S, int h0, int n,
+                             int64_t Sp, float* D, float* lse_c,
+                             hipStream_t st);
+
+// ---- attention forward (attn_fwd.hip) ------------------------------------
+// Qc [U, Sp, d], Kp [Hkv, Sp, d], Vt [Hkv, d, Sp] (MFMA order) -> Oc [U, Sp, d]
+// and lse rows h0..h0+U-1 of the caller's [Hq, S] array.
+hipError_t launch_attn_fwd(const bf16* Qc, const bf16* Kp, const bf16* Vt,
+                           bf16* Oc, float* lse, int64_t S, int64_t Sp, int U,
+                           int h0, int G, int causal, hipStream_t st);
+
+// ---- attention backward (attn_bwd.hip) -----------------------------------
+// Key/value gradients of the chunk's heads, accumulated in fp32 on top of
+// dK32/dV32 [Hkv, Sp, d] (read unless the chunk holds a group's first head),
+// written back there, or -- when the chunk holds the group's last head --
+// scaled and rounded into dk/dv bf16 [S, Hkv, d].
+hipError_t launch_attn_bwd_dkdv(const bf16* Qc, const bf16* Qct,
+                                const bf16* dOc, const bf16* dOct,
+                                const float* lse_c, const float* D,
+                                const bf16* Kp, const bf16* Vp, float* dK32,
+                                float* dV32, bf16* dk, bf16* dv, int64_t S,
+                                int64_t Sp, int U, int h0, int G, int Hkv,
+                                int causal, hipStream_t st);
+// dQc [U, Sp, d] of the chunk's heads.
+hipError_t launch_attn_bwd_dq(const bf16* Qc, const bf16* dOc,
+                              const float* lse_c, const float* D,
+                              const bf16* Kp, const bf16* Kt, const bf16* Vp,
+                              bf16* dQc, int64_t S, int64_t Sp, int U, int h0,
+                              int G, int causal, hipStream_t st);
+
+}  // namespace upipe

@@ -1,0 +1,128 @@
+// Layout kernels: the one-GPU stand-ins for UPipe's all-to-all buffers.
+//
+// In the paper (Section 3.3, Appendix A) each stage's query/key/value heads
+// arrive through inp_all_to_all into head-distributed buffers [S, U/C, d],
+// and the stage output leaves through out_all_to_all into its slot of the
+// preallocated `final_out`.  On one GPU these become:
+//   pack   token-major [S, H, d] (chosen heads)  ->  head-major [n, Sp, d]
+//          (+ optionally the transposed copy [n, d, Sp] in MFMA order)
+//   unpack head-major [n, Sp, d]                 ->  token-major [S, H, d]
+// Rows S..Sp-1 of packed buffers are zero, so the attention kernels never
+// test sequence bounds on loads.  All kernels are HBM-bound copies.
+#include "common.h"
+#include "kernels.h"
+
+namespace upipe {
+
+// One workgroup packs a 64-row slab of one head.  256 threads, each moving
+// four 16-byte pieces; the transposed copy goes through LDS.
+__global__ __launch_bounds__(256) void pack_rows_kernel(
+    const bf16* __restrict__ src, int64_t S, int H, int h0, int64_t Sp,
+    bf16* __restrict__ dst, bf16* __restrict__ dst_t) {
+  __shared__ __attribute__((aligned(16))) bf16 tile[64][HEAD_DIM + 8];
+  const int t = threadIdx.x;
+  const int hh = blockIdx.y;
+  const int64_t s0 = (int64_t)blockIdx.x * 64;
+  const int h = h0 + hh;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int pi = t + 256 * r;
+    const int row = pi >> 4, chunk = pi & 15;
+    const int64_t s = s0 + row;
+    u32x4 val = {0u, 0u, 0u, 0u};
+    if (s < S)
+      val = *reinterpret_cast<const u32x4*>(src + (s * H + h) * HEAD_DIM + chunk * 8);
+    if (dst)
+      *reinterpret_cast<u32x4*>(dst + ((int64_t)hh * Sp + s) * HEAD_DIM + chunk * 8) = val;
+    if (dst_t) *reinterpret_cast<u32x4*>(&tile[row][chunk * 8]) = val;
+  }
+  if (!dst_t) return;
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int pi = t + 256 * r;
+    const int drow = pi >> 3, c = pi & 7;
+    bf16x8 out;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) out[j] = tile[perm16(8 * c + j)][drow];
+    *reinterpret_cast<bf16x8*>(dst_t + ((int64_t)hh * HEAD_DIM + drow) * Sp + s0 + 8 * c) = out;
+  }
+}
+
+// Copies rows [0, S) of head-major [n, Sp, d] into heads h0.. of [S, H, d].
+__global__ __launch_bounds__(256) void unpack_rows_kernel(
+    const bf16* __restrict__ src, int64_t S, int H, int h0, int n, int64_t Sp,
+    bf16* __restrict__ dst) {
+  const int64_t pieces = S * n * 16;
+  for (int64_t pi = (int64_t)blockIdx.x * 256 + threadIdx.x; pi < pieces;
+       pi += (int64_t)gridDim.x * 256) {
+    const int chunk = pi & 15;
+    const int64_t rest = pi >> 4;
+    const int hh = rest % n;
+    const int64_t s = rest / n;
+    const u32x4 val = *reinterpret_cast<const u32x4*>(
+        src + ((int64_t)hh * Sp + s) * HEAD_DIM + chunk * 8);
+    *reinterpret_cast<u32x4*>(dst + (s * H + h0 + hh) * HEAD_DIM + chunk * 8) = val;
+  }
+}
+
+// D[hh][s] = sum_e dO(s, hh, e) * O(s, hh, e) in fp32 (the backward's row
+// term) and the chunk's log-sum-exp rows copied to a padded buffer.  Element
+// (s, hh, e) of an operand X lives at X + s * x_row + hh * x_head + e.  One
+// wave per (row, head); lanes hold two elements each and reduce by shuffles.
+__global__ __launch_bounds__(256) void rowdot_lse_kernel(
+    const bf16* __restrict__ a, int64_t a_row, int64_t a_head,
+    const bf16* __restrict__ b, int64_t b_row, int64_t b_head,
+    const float* __restrict__ lse, int64_t S, int h0, int n, int64_t Sp,
+    float* __restrict__ D, float* __restrict__ lse_c) {
+  const int lane = threadIdx.x & 63;
+  const int64_t task = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (task >= (int64_t)n * Sp) return;
+  const int hh = task / Sp;
+  const int64_t s = task % Sp;
+  float acc = 0.f, l = 0.f;
+  if (s < S) {
+    const bf16* pa = a + s * a_row + hh * a_head + 2 * lane;
+    const bf16* pb = b + s * b_row + hh * b_head + 2 * lane;
+    acc = (float)pa[0] * (float)pb[0] + (float)pa[1] * (float)pb[1];
+    l = lse[(int64_t)(h0 + hh) * S + s];
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) acc += __shfl_xor(acc, off);
+  if (lane == 0) {
+    D[(int64_t)hh * Sp + s] = acc;
+    lse_c[(int64_t)hh * Sp + s] = l;
+  }
+}
+
+hipError_t launch_pack_rows(const bf16* src, int64_t S, int H, int h0, int n,
+                            int64_t Sp, bf16* dst, bf16* dst_t, hipStream_t st) {
+  dim3 grid((unsigned)(Sp / 64), (unsigned)n);
+  hipLaunchKernelGGL(pack_rows_kernel, grid, dim3(256), 0, st, src, S, H, h0,
+                     Sp, dst, dst_t);
+  return hipGetLastError();
+}
+
+hipError_t launch_unpack_rows(const bf16* src, int64_t S, int H, int h0, int n,
+                              int64_t Sp, bf16* dst, hipStream_t st) {
+  const int64_t pieces = S * n * 16;
+  int64_t blocks = (pieces + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  hipLaunchKernelGGL(unpack_rows_kernel, dim3((unsigned)blocks), dim3(256), 0,
+                     st, src, S, H, h0, n, Sp, dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_rowdot_lse(const bf16* a, int64_t a_row, int64_t a_head,
+                             const bf16* b, int64_t b_row, int64_t b_head,
+                             const float* lse, int64_t S, int h0, int n,
+                             int64_t Sp, float* D, float* lse_c,
+                             hipStream_t st) {
+  const int64_t tasks = (int64_t)n * Sp;
+  hipLaunchKernelGGL(rowdot_lse_kernel, dim3((unsigned)((tasks + 3) / 4)),
+                     dim3(256), 0, st, a, a_row, a_head, b, b_row, b_head, lse,
+                     S, h0, n, Sp, D, lse_c);
+  return hipGetLastError();
+}
+
+}  // namespace upipe

@@ -1,0 +1,295 @@
+"""ctypes binding of libupipe.so (the C ABI in include/upipe.h).
+
+Argument marshalling only: every step of the path runs in the library's HIP
+kernels.  PyTorch supplies device memory and the current stream.  The
+``upipe_*`` functions mirror the C entry points one to one; ``attn_fwd`` /
+``attn_bwd`` / ``layer_fwd`` / ``layer_bwd`` are conveniences that allocate
+outputs and the workspace with torch and raise on a non-zero status.
+
+If the library has not been built this module raises when it is first used;
+there is no fallback implementation.
+"""
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libupipe.so")
+
+UPIPE_OK = 0
+STATUS = {0: "UPIPE_OK", -1: "UPIPE_ERR_INVALID_ARG", -2: "UPIPE_ERR_UNSUPPORTED",
+          -3: "UPIPE_ERR_WORKSPACE", -4: "UPIPE_ERR_HIP"}
+
+_c_void_p = ctypes.c_void_p
+_i64 = ctypes.c_int64
+_int = ctypes.c_int
+_size = ctypes.c_size_t
+_fptr = ctypes.c_void_p
+
+_SIGNATURES = {
+    "upipe_status_string": (ctypes.c_char_p, [_int]),
+    "upipe_version": (_int, []),
+    "upipe_gqa_schedule": (_int, [_int, _int, _int, _int,
+                                  ctypes.POINTER(_int), ctypes.POINTER(_int)]),
+    "upipe_attn_fwd_workspace_size": (_size, [_i64, _int, _int, _int, _int]),
+    "upipe_attn_bwd_workspace_size": (_size, [_i64, _int, _int, _int, _int]),
+    "upipe_layer_fwd_workspace_size": (_size, [_i64, _int, _int, _int, _int, _int]),
+    "upipe_layer_bwd_workspace_size": (_size, [_i64, _int, _int, _int, _int, _int]),
+    "upipe_attn_fwd": (_int, [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _fptr,
+                              _i64, _int, _int, _int, _int, _int,
+                              _c_void_p, _size, _c_void_p]),
+    "upipe_attn_bwd": (_int, [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _fptr,
+                              _c_void_p, _c_void_p, _c_void_p, _c_void_p,
+                              _i64, _int, _int, _int, _int, _int,
+                              _c_void_p, _size, _c_void_p]),
+    "upipe_layer_fwd": (_int, [_c_void_p, _c_void_p, _c_void_p, _c_void_p,
+                               _c_void_p, _fptr, _i64, _int, _int, _int, _int,
+                               _int, _c_void_p, _size, _c_void_p]),
+    "upipe_layer_bwd": (_int, [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _fptr,
+                               _c_void_p, _c_void_p, _c_void_p, _c_void_p,
+                               _i64, _int, _int, _int, _int, _int,
+                               _c_void_p, _size, _c_void_p]),
+    "upipe_profile_enable": (_int, [_int]),
+    "upipe_profile_reset": (_int, []),
+    "upipe_profile_query": (_int, [ctypes.c_char_p, ctypes.POINTER(_int),
+                                   ctypes.POINTER(ctypes.c_double)]),
+    "upipe_profile_name": (ctypes.c_char_p, [_int]),
+}
+
+_lib = None
+
+
+def lib():
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                f"{LIB_PATH} is missing: build it with "
+                "`python -m paper_2602_21196_amd.build` (no fallback exists)")
+        handle = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGNATURES.items():
+            fn = getattr(handle, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = handle
+    return _lib
+
+
+class UpipeError(RuntimeError):
+    def __init__(self, fn, status):
+        super().__init__(f"{fn} returned {STATUS.get(status, status)}")
+        self.status = status
+
+
+def _check(fn, status):
+    if status != UPIPE_OK:
+        raise UpipeError(fn, status)
+
+
+# ------------------------------------------------------------ raw mirrors
+
+def upipe_status_string(status):
+    return lib().upipe_status_string(status).decode()
+
+
+def upipe_version():
+    return lib().upipe_version()
+
+
+def upipe_gqa_schedule(H, Hkv, C, U):
+    """Returns (status, stage_heads list[H], kv_stage list[Hkv])."""
+    heads = (_int * max(H, 1))()
+    kvs = (_int * max(Hkv, 1))()
+    st = lib().upipe_gqa_schedule(H, Hkv, C, U, heads, kvs)
+    return st, list(heads)[:H], list(kvs)[:Hkv]
+
+
+def upipe_attn_fwd_workspace_size(S, Hq, Hkv, d, U):
+    return lib().upipe_attn_fwd_workspace_size(S, Hq, Hkv, d, U)
+
+
+def upipe_attn_bwd_workspace_size(S, Hq, Hkv, d, U):
+    return lib().upipe_attn_bwd_workspace_size(S, Hq, Hkv, d, U)
+
+
+def upipe_layer_fwd_workspace_size(S, d_model, Hq, Hkv, d, U):
+    return lib().upipe_layer_fwd_workspace_size(S, d_model, Hq, Hkv, d, U)
+
+
+def upipe_layer_bwd_workspace_size(S, d_model, Hq, Hkv, d, U):
+    return lib().upipe_layer_bwd_workspace_size(S, d_model, Hq, Hkv, d, U)
+
+
+def upipe_attn_fwd(q, k, v, o, lse, S, Hq, Hkv, d, causal, U, ws, ws_bytes,
+                   stream):
+    return lib().upipe_attn_fwd(q, k, v, o, lse, S, Hq, Hkv, d, causal, U, ws,
+                                ws_bytes, stream)
+
+
+def upipe_attn_bwd(q, k, v, o, lse, dout, dq, dk, dv, S, Hq, Hkv, d, causal,
+                   U, ws, ws_bytes, stream):
+    return lib().upipe_attn_bwd(q, k, v, o, lse, dout, dq, dk, dv, S, Hq, Hkv,
+                                d, causal, U, ws, ws_bytes, stream)
+
+
+def upipe_layer_fwd(x, wqkv, wo, y, o_saved, lse_saved, S, d_model, Hq, Hkv,
+                    d, U, ws, ws_bytes, stream):
+    return lib().upipe_layer_fwd(x, wqkv, wo, y, o_saved, lse_saved, S,
+                                 d_model, Hq, Hkv, d, U, ws, ws_bytes, stream)
+
+
+def upipe_layer_bwd(x, wqkv, wo, o_saved, lse_saved, dy, dx, dwqkv, dwo, S,
+                    d_model, Hq, Hkv, d, U, ws, ws_bytes, stream):
+    return lib().upipe_layer_bwd(x, wqkv, wo, o_saved, lse_saved, dy, dx,
+                                 dwqkv, dwo, S, d_model, Hq, Hkv, d, U, ws,
+                                 ws_bytes, stream)
+
+
+def upipe_profile_enable(on):
+    return lib().upipe_profile_enable(int(on))
+
+
+def upipe_profile_reset():
+    return lib().upipe_profile_reset()
+
+
+def upipe_profile_query(name):
+    n = _int(0)
+    ms = ctypes.c_double(0.0)
+    st = lib().upipe_profile_query(name.encode(), ctypes.byref(n),
+                                   ctypes.byref(ms))
+    _check("upipe_profile_query", st)
+    return n.value, ms.value
+
+
+def upipe_profile_names():
+    out, i = [], 0
+    while True:
+        nm = lib().upipe_profile_name(i)
+        if nm is None:
+            return out
+        out.append(nm.decode())
+        i += 1
+
+
+# ------------------------------------------------------ torch conveniences
+
+def _torch():
+    import torch
+    return torch
+
+
+def _ptr(t, dtype, name):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must live on the GPU")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+def _stream():
+    return _torch().cuda.current_stream().cuda_stream
+
+
+def workspace(nbytes, device):
+    torch = _torch()
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
+def attn_fwd(q, k, v, causal=True, U=1, ws=None):
+    """o [S,Hq,d] bf16, lse [Hq,S] fp32 for q [S,Hq,d], k/v [S,Hkv,d] bf16."""
+    torch = _torch()
+    S, Hq, d = q.shape
+    Hkv = k.shape[1]
+    need = upipe_attn_fwd_workspace_size(S, Hq, Hkv, d, U)
+    if need == 0:
+        raise UpipeError("upipe_attn_fwd_workspace_size", -1)
+    if ws is None:
+        ws = workspace(need, q.device)
+    o = torch.empty_like(q)
+    lse = torch.empty((Hq, S), dtype=torch.float32, device=q.device)
+    bf = torch.bfloat16
+    st = upipe_attn_fwd(_ptr(q, bf, "q"), _ptr(k, bf, "k"), _ptr(v, bf, "v"),
+                        _ptr(o, bf, "o"), _ptr(lse, torch.float32, "lse"),
+                        S, Hq, Hkv, d, int(causal), U, ws.data_ptr(),
+                        ws.numel(), _stream())
+    _check("upipe_attn_fwd", st)
+    return o, lse
+
+
+def attn_bwd(q, k, v, o, lse, dout, causal=True, U=1, ws=None):
+    """dq [S,Hq,d], dk, dv [S,Hkv,d] bf16."""
+    torch = _torch()
+    S, Hq, d = q.shape
+    Hkv = k.shape[1]
+    need = upipe_attn_bwd_workspace_size(S, Hq, Hkv, d, U)
+    if need == 0:
+        raise UpipeError("upipe_attn_bwd_workspace_size", -1)
+    if ws is None:
+        ws = workspace(need, q.device)
+    dq = torch.empty_like(q)
+    dk = torch.empty_like(k)
+    dv = torch.empty_like(v)
+    bf = torch.bfloat16
+    st = upipe_attn_bwd(_ptr(q, bf, "q"), _ptr(k, bf, "k"), _ptr(v, bf, "v"),
+                        _ptr(o, bf, "o"), _ptr(lse, torch.float32, "lse"),
+                        _ptr(dout, bf, "dout"), _ptr(dq, bf, "dq"),
+                        _ptr(dk, bf, "dk"), _ptr(dv, bf, "dv"),
+                        S, Hq, Hkv, d, int(causal), U, ws.data_ptr(),
+                        ws.numel(), _stream())
+    _check("upipe_attn_bwd", st)
+    return dq, dk, dv
+
+
+def layer_fwd(x, wqkv, wo, Hq, Hkv, d=128, U=1, ws=None):
+    """y [S,dm] bf16, o_saved [S,Hq,d] bf16, lse_saved [Hq,S] fp32."""
+    torch = _torch()
+    S, dm = x.shape
+    need = upipe_layer_fwd_workspace_size(S, dm, Hq, Hkv, d, U)
+    if need == 0:
+        raise UpipeError("upipe_layer_fwd_workspace_size", -1)
+    if ws is None:
+        ws = workspace(need, x.device)
+    y = torch.empty_like(x)
+    o = torch.empty((S, Hq, d), dtype=torch.bfloat16, device=x.device)
+    lse = torch.empty((Hq, S), dtype=torch.float32, device=x.device)
+    bf = torch.bfloat16
+    st = upipe_layer_fwd(_ptr(x, bf, "x"), _ptr(wqkv, bf, "wqkv"),
+                         _ptr(wo, bf, "wo"), _ptr(y, bf, "y"),
+                         _ptr(o, bf, "o_saved"),
+                         _ptr(lse, torch.float32, "lse_saved"),
+                         S, dm, Hq, Hkv, d, U, ws.data_ptr(), ws.numel(),
+                         _stream())
+    _check("upipe_layer_fwd", st)
+    return y, o, lse
+
+
+def layer_bwd(x, wqkv, wo, o_saved, lse_saved, dy, Hq, Hkv, d=128, U=1,
+              ws=None):
+    """dx [S,dm], dwqkv [dm,(Hq+2Hkv)d], dwo [Hq d, dm], all bf16."""
+    torch = _torch()
+    S, dm = x.shape
+    need = upipe_layer_bwd_workspace_size(S, dm, Hq, Hkv, d, U)
+    if need == 0:
+        raise UpipeError("upipe_layer_bwd_workspace_size", -1)
+    if ws is None:
+        ws = workspace(need, x.device)
+    dx = torch.empty_like(x)
+    dwqkv = torch.empty_like(wqkv)
+    dwo = torch.empty_like(wo)
+    bf = torch.bfloat16
+    st = upipe_layer_bwd(_ptr(x, bf, "x"), _ptr(wqkv, bf, "wqkv"),
+                         _ptr(wo, bf, "wo"), _ptr(o_saved, bf, "o_saved"),
+                         _ptr(lse_saved, torch.float32, "lse_saved"),
+                         _ptr(dy, bf, "dy"), _ptr(dx, bf, "dx"),
+                         _ptr(dwqkv, bf, "dwqkv"), _ptr(dwo, bf, "dwo"),
+                         S, dm, Hq, Hkv, d, U, ws.data_ptr(), ws.numel(),
+                         _stream())
+    _check("upipe_layer_bwd", st)
+    return dx, dwqkv, dwo

@@ -1,0 +1,117 @@
+"""The C ABI on the host: it loads, exports what the header declares, and
+validates arguments before any GPU work (no kernel is launched here)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from oracle import schedule as SCH
+from paper_2602_21196_amd import upipe
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "upipe.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(upipe_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_library_loads_and_exports_every_declared_symbol():
+    lib = upipe.lib()
+    names = _declared()
+    assert len(names) >= 15
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in upipe.h but not exported"
+        assert n in upipe._SIGNATURES, f"{n} has no Python mirror"
+
+
+def test_status_strings_and_version():
+    assert upipe.upipe_status_string(0) == "UPIPE_OK"
+    assert upipe.upipe_status_string(-3) == "UPIPE_ERR_WORKSPACE"
+    assert upipe.upipe_status_string(7) == "UPIPE_ERR_UNKNOWN"
+    assert upipe.upipe_version() >= 100
+    assert "attn_fwd" in upipe.upipe_profile_names()
+
+
+FAKE = 1 << 20   # a 16-byte aligned non-null address; never dereferenced
+
+
+def _fwd(**kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=FAKE, S=512, Hq=4, Hkv=1,
+             d=128, causal=1, U=1, ws=FAKE, ws_bytes=1 << 40, stream=None)
+    a.update(kw)
+    return upipe.upipe_attn_fwd(*a.values())
+
+
+def _bwd(**kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=FAKE, dout=FAKE, dq=FAKE,
+             dk=FAKE, dv=FAKE, S=512, Hq=4, Hkv=1, d=128, causal=1, U=1,
+             ws=FAKE, ws_bytes=1 << 40, stream=None)
+    a.update(kw)
+    return upipe.upipe_attn_bwd(*a.values())
+
+
+@pytest.mark.parametrize("fn", [_fwd, _bwd])
+def test_argument_validation(fn):
+    INV, UNS, WS = -1, -2, -3
+    assert fn(S=0) == INV
+    assert fn(Hq=4, Hkv=3) == INV             # Hkv does not divide Hq
+    assert fn(U=3) == INV                     # U does not divide Hq
+    assert fn(U=0) == INV
+    assert fn(d=64) == UNS
+    assert fn(Hq=128, Hkv=1, U=1) == UNS
+    assert fn(q=None) == INV
+    assert fn(q=FAKE + 8) == INV              # misaligned
+    assert fn(ws=None) == INV
+    assert fn(causal=2) == INV
+    assert fn(ws_bytes=1024) == WS
+
+
+def test_workspace_sizes_follow_the_plan():
+    S, d = 131072, 128
+    Sp = S
+    head = Sp * d * 2
+    for U in (1, 2, 4):
+        fwd = upipe.upipe_attn_fwd_workspace_size(S, 4, 1, d, U)
+        assert fwd == 2 * head + 2 * U * head
+        bwd = upipe.upipe_attn_bwd_workspace_size(S, 4, 1, d, U)
+        carry = 4 * head if U < 4 else 0          # fp32 dK, dV accumulators
+        assert bwd == 3 * head + carry + 5 * U * head + 2 * U * Sp * 4
+    # padding of a ragged length to the 128-row granule
+    assert upipe.upipe_attn_fwd_workspace_size(1, 1, 1, d, 1) == 4 * 128 * d * 2
+    assert upipe.upipe_attn_fwd_workspace_size(0, 1, 1, d, 1) == 0
+    assert upipe.upipe_attn_fwd_workspace_size(5, 4, 1, 64, 1) == 0
+    # memory grows linearly in U
+    sizes = [upipe.upipe_attn_fwd_workspace_size(S, 8, 1, d, U)
+             for U in (1, 2, 4, 8)]
+    assert sizes[1] - sizes[0] == (sizes[2] - sizes[1]) // 2 == \
+        (sizes[3] - sizes[2]) // 4
+
+
+@pytest.mark.parametrize("H,Hkv,C,U", [(16, 4, 4, 4), (32, 8, 8, 8),
+                                       (64, 8, 8, 8), (64, 16, 4, 8),
+                                       (32, 8, 8, 16), (8, 2, 2, 2)])
+def test_gqa_schedule_matches_oracle(H, Hkv, C, U):
+    st, heads, kv = upipe.upipe_gqa_schedule(H, Hkv, C, U)
+    assert st == 0
+    stages, kv_stage = SCH.gqa_schedule(H, Hkv, C, U)
+    assert heads == [h for s in stages for h in s]
+    assert kv == kv_stage
+
+
+def test_gqa_schedule_rejects_bad_shapes():
+    assert upipe.upipe_gqa_schedule(16, 4, 4, 6)[0] == -1
+    assert upipe.upipe_gqa_schedule(16, 4, 3, 3)[0] == -1
+    assert upipe.upipe_gqa_schedule(0, 4, 4, 4)[0] == -1
+
+
+def test_layer_entry_points_validate():
+    S, dm = 256, 512
+    assert upipe.upipe_layer_fwd_workspace_size(S, 500, 4, 1, 128, 1) == 0
+    assert upipe.upipe_layer_fwd_workspace_size(S, dm, 4, 1, 64, 1) == 0
+    assert upipe.upipe_layer_fwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, S, dm, 4,
+                                 1, 128, 3, FAKE, 1 << 40, None) == -1
