@@ -1,0 +1,203 @@
+"""Benchmark: head-chunked causal GQA attention fwd+bwd on one MI355X.
+
+One step = one pass of the whole hot path over one batch of synthetic input:
+upipe_attn_fwd followed by upipe_attn_bwd (pack, flash forward, unpack,
+backward pre-pass, dK/dV, dQ, unpack, for every head chunk) on the
+Llama3-8B per-GPU share at 8-way Ulysses (S = 131072, 4 query heads, 1 kv
+head, d = 128), inputs resident in HBM.  Prints one JSON line.
+
+Throughput counts only algorithmic work: 4 d flops per visible causal
+(query, key, head) triple for the forward and 2.5x that for the backward.
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = ("attention fwd+bwd TFLOP/s (causal) per MI355X; "
+          "peak activation GB vs chunk size U")
+PEAK_BF16_TFLOPS = 2516.6   # 256 CU x 4096 flop/clk x 2.4 GHz, dense bf16
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=5)
+    p.add_argument("--warmup", type=int, default=2)
+    p.add_argument("--workload", default="llama8b_share")
+    p.add_argument("--U", type=int, default=1)
+    p.add_argument("--no-sweep", action="store_true",
+                   help="skip the per-U throughput/memory sweep")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-seconds", type=float, default=15.0,
+                   help="target CPU time of the oracle sample")
+    return p.parse_args()
+
+
+def kernel_flops(S, U, d, causal=True):
+    """Algorithmic flops per launch of each attention kernel (one chunk)."""
+    pairs = S * (S + 1) // 2 if causal else S * S
+    return {
+        "attn_fwd": 4 * d * U * pairs,          # Q K^T and P V
+        "attn_bwd_dkdv": 8 * d * U * pairs,     # S, dP recompute + dV, dK
+        "attn_bwd_dq": 2 * d * U * pairs,       # dQ (S, dP recomputed again)
+    }
+
+
+def cpu_baseline(w, q, k, v, do, target_s):
+    """Oracle (float64 numpy) on a bounded causal prefix of the workload.
+
+    The first S' tokens of a causal sequence form a causal attention problem
+    of their own with exactly the same rows; the oracle runs forward and
+    backward for one query head on that prefix and its rate is reported in
+    the metric's unit (TFLOP/s of algorithmic work).
+    """
+    import numpy as np
+    from oracle import attention as A
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        cores = os.cpu_count()
+
+    def run(sp):
+        f = lambda t, h: t[:sp, :h].float().double().numpy()  # noqa: E731
+        args = (f(q, 1), f(k, 1), f(v, 1), f(do, 1))
+        t0 = time.perf_counter()
+        A.attn_fwd(*args[:3])
+        A.attn_bwd(*args)
+        return time.perf_counter() - t0
+
+    sp = 2048
+    t = run(sp)
+    # time grows ~ S'^2; aim for target_s
+    scale = (target_s / max(t, 1e-3)) ** 0.5
+    sp = int(min(w.S, max(2048, (sp * scale) // 128 * 128)))
+    t = run(sp)
+    pairs = sp * (sp + 1) // 2
+    flops = 3.5 * 4 * w.d * pairs
+    return {"value": round(flops / t / 1e12, 6), "unit": "TFLOP/s",
+            "cores": cores, "kind": "oracle",
+            "sample": f"causal prefix S'={sp} of {w.name}, 1 query head "
+                      f"(kv head 0), fwd+bwd, float64 numpy, {t:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: this build has no multi-GPU "
+              f"path (asked for --gpus {args.gpus}).", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import workloads as W
+    from paper_2602_21196_amd import upipe
+
+    w = W.WORKLOADS[args.workload]
+    if w.is_layer:
+        print("bench.py times the attention workloads", file=sys.stderr)
+        sys.exit(2)
+    dev = "cuda:0"
+    S, Hq, Hkv, d, U = w.S, w.Hq, w.Hkv, w.d, args.U
+    q, k, v, do = W.attention_inputs(S, Hq, Hkv, d, w.seed)
+    qd, kd, vd, dod = (t.to(dev) for t in (q, k, v, do))
+    fwd_flops, bwd_flops = W.attention_flops(S, Hq, d)
+    step_flops = fwd_flops + bwd_flops
+
+    ws_f = upipe.workspace(upipe.upipe_attn_fwd_workspace_size(S, Hq, Hkv, d, U), dev)
+    ws_b = upipe.workspace(upipe.upipe_attn_bwd_workspace_size(S, Hq, Hkv, d, U), dev)
+
+    def step():
+        o, lse = upipe.attn_fwd(qd, kd, vd, causal=True, U=U, ws=ws_f)
+        upipe.attn_bwd(qd, kd, vd, o, lse, dod, causal=True, U=U, ws=ws_b)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    upipe.upipe_profile_reset()
+    upipe.upipe_profile_enable(1)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    upipe.upipe_profile_enable(0)
+    ms_per_step = elapsed / args.steps * 1e3
+    value = step_flops / (elapsed / args.steps) / 1e12
+
+    kflops = kernel_flops(S, U, d)
+    kernels = {}
+    for name in upipe.upipe_profile_names():
+        n, ms = upipe.upipe_profile_query(name)
+        if n == 0:
+            continue
+        entry = {"launches_per_step": n // args.steps,
+                 "ms_per_step": round(ms / args.steps, 4),
+                 "avg_launch_ms": round(ms / n, 4)}
+        if name in kflops:
+            entry["tflops"] = round(kflops[name] / (ms / n / 1e3) / 1e12, 2)
+        kernels[name] = entry
+    dom = max(kernels, key=lambda n: kernels[n]["ms_per_step"])
+    achieved = kernels[dom].get("tflops")
+    roofline = {"kernel": dom, "bound": "mfma",
+                "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4) if achieved else None,
+                "traffic": None}
+    upipe.upipe_profile_reset()
+
+    out = {"metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s",
+           "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+           "ms_per_step": round(ms_per_step, 3), "higher_is_better": True,
+           "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+           "data": "synthetic",
+           "config": {"workload": w.name, "S": S, "Hq": Hq, "Hkv": Hkv,
+                      "d": d, "U": U, "causal": True, "seed": w.seed},
+           "frac_of_peak": round(value / PEAK_BF16_TFLOPS, 4),
+           "roofline": roofline, "kernels": kernels}
+
+    if not args.no_sweep:
+        del ws_f, ws_b
+        torch.cuda.synchronize()
+        # outputs of one fwd+bwd: o, dq [S,Hq,d] bf16, dk, dv [S,Hkv,d] bf16,
+        # lse [Hq,S] fp32; everything else allocated in between is workspace.
+        out_bytes = 2 * (2 * S * Hq * d) + 2 * (2 * S * Hkv * d) + 4 * Hq * S
+        sweep_mem, sweep_tf = {}, {}
+        for u in w.U_sweep:
+            torch.cuda.empty_cache()
+            torch.cuda.reset_peak_memory_stats()
+            base = torch.cuda.memory_allocated()
+            o, lse = upipe.attn_fwd(qd, kd, vd, U=u)
+            g = upipe.attn_bwd(qd, kd, vd, o, lse, dod, U=u)
+            torch.cuda.synchronize()
+            peak = torch.cuda.max_memory_allocated() - base
+            sweep_mem[str(u)] = round((peak - out_bytes) / 1e9, 4)
+            del o, lse, g
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            for _ in range(2):
+                o, lse = upipe.attn_fwd(qd, kd, vd, U=u)
+                g = upipe.attn_bwd(qd, kd, vd, o, lse, dod, U=u)
+            torch.cuda.synchronize()
+            sweep_tf[str(u)] = round(step_flops / ((time.perf_counter() - t1) / 2) / 1e12, 2)
+            del o, lse, g
+        out["peak_activation_gb_vs_U"] = sweep_mem
+        out["peak_activation_note"] = (
+            "max_memory_allocated during one fwd+bwd above the resident "
+            "inputs, minus the outputs o, lse, dq, dk, dv: the workspaces")
+        out["tflops_vs_U"] = sweep_tf
+
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, q, k, v, do, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,121 @@
+"""GPU parity of the attention block (QKV projection slice, attention,
+output-projection accumulation, and the backward with recomputation)."""
+
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from oracle import attention as A
+from oracle import layer as L
+from tol import as64, assert_close
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def _upipe():
+    from paper_2602_21196_amd import upipe
+    upipe.lib()
+    return upipe
+
+
+def _bits_equal(a, b):
+    if a.dtype == torch.bfloat16:
+        return torch.equal(a.view(torch.int16), b.view(torch.int16))
+    return torch.equal(a.view(torch.int32), b.view(torch.int32))
+
+
+def _run(x, wqkv, wo, dy, Hq, Hkv, U):
+    up = _upipe()
+    xd, wd, wod, dyd = (t.to(DEV) for t in (x, wqkv, wo, dy))
+    y, o, lse = up.layer_fwd(xd, wd, wod, Hq, Hkv, U=U)
+    dx, dw, dwo = up.layer_bwd(xd, wd, wod, o, lse, dyd, Hq, Hkv, U=U)
+    torch.cuda.synchronize()
+    return [t.cpu() for t in (y, o, lse, dx, dw, dwo)]
+
+
+NAMES = ("y", "o_saved", "lse", "dx", "dwqkv", "dwo")
+RMS = (False, False, False, False, True, True)
+
+
+def _blocks(Hq, Hkv):
+    """Per-output-block scales: the Q, K, V column groups of dWqkv."""
+    d = 128
+    return (None, None, None, None,
+            [slice(0, Hq * d), slice(Hq * d, (Hq + Hkv) * d),
+             slice((Hq + Hkv) * d, (Hq + 2 * Hkv) * d)], None)
+
+
+@pytest.mark.parametrize("S,dm,Hq,Hkv", [(300, 256, 4, 1), (513, 384, 4, 2),
+                                         (128, 128, 2, 2), (1, 256, 2, 1)])
+def test_layer_small_all_chunk_sizes(S, dm, Hq, Hkv):
+    x, wqkv, wo, dy = W.layer_inputs(S, dm, Hq, Hkv, 128, 40 + S)
+    x64, w64, wo64, dy64 = (as64(t) for t in (x, wqkv, wo, dy))
+    y, o, lse = L.layer_fwd(x64, w64, wo64, Hq, Hkv, 128)
+    dx, dw, dwo = L.layer_bwd(x64, w64, wo64, dy64, Hq, Hkv, 128)
+    ref = (y, o, lse, dx, dw, dwo)
+    first = None
+    for U in [u for u in range(1, Hq + 1) if Hq % u == 0]:
+        print(f"layer S={S} dm={dm} Hq={Hq} Hkv={Hkv} U={U}", flush=True)
+        got = _run(x, wqkv, wo, dy, Hq, Hkv, U)
+        for name, g, r, rs, bl in zip(NAMES, got, ref, RMS, _blocks(Hq, Hkv)):
+            assert_close(f"{name} U={U}", g, r, rms_scaled=rs, blocks=bl)
+        if first is None:
+            first = got
+        else:
+            for name, a, b in zip(NAMES, first, got):
+                assert _bits_equal(a, b), f"{name}: U=1 vs U={U}"
+
+
+@pytest.mark.timeout(300)
+def test_layer_llama_width_short_sequence():
+    """d_model = 4096 as in the Llama3-8B layer share, S short enough for the
+    full oracle: every output including the weight gradients."""
+    S, dm, Hq, Hkv = 2048, 4096, 4, 1
+    x, wqkv, wo, dy = W.layer_inputs(S, dm, Hq, Hkv, 128, 7)
+    x64, w64, wo64, dy64 = (as64(t) for t in (x, wqkv, wo, dy))
+    y, o, lse = L.layer_fwd(x64, w64, wo64, Hq, Hkv, 128)
+    dx, dw, dwo = L.layer_bwd(x64, w64, wo64, dy64, Hq, Hkv, 128)
+    got = {}
+    for U in (1, 4):
+        got[U] = _run(x, wqkv, wo, dy, Hq, Hkv, U)
+    for name, g, r, rs, bl in zip(NAMES, got[1], (y, o, lse, dx, dw, dwo), RMS,
+                                  _blocks(Hq, Hkv)):
+        assert_close(name, g, r, rms_scaled=rs, blocks=bl)
+    for name, a, b in zip(NAMES, got[1], got[4]):
+        assert _bits_equal(a, b), name
+
+
+@pytest.mark.timeout(900)
+def test_llama8b_layer_share_sampled():
+    w = W.WORKLOADS["llama8b_layer"]
+    S, dm, Hq, Hkv, d = w.S, w.d_model, w.Hq, w.Hkv, w.d
+    x, wqkv, wo, dy = W.layer_inputs(S, dm, Hq, Hkv, d, w.seed)
+    outs = {}
+    for U in w.U_sweep:
+        print(f"llama8b_layer S={S} U={U}", flush=True)
+        outs[U] = _run(x, wqkv, wo, dy, Hq, Hkv, U)
+    for U in w.U_sweep[1:]:
+        for name, a, b in zip(NAMES, outs[1], outs[U]):
+            assert _bits_equal(a, b), f"{name}: U=1 vs U={U}"
+    y, o, lse, dx, dwqkv, dwo = outs[1]
+    x64, w64, wo64, dy64 = (as64(t) for t in (x, wqkv, wo, dy))
+    rows = W.sample_rows(S, 128, w.seed)
+    print("oracle sampled rows", flush=True)
+    y_r, o_r, lse_r = L.layer_fwd_rows(x64, w64, wo64, Hq, Hkv, d, rows)
+    assert_close("y rows", y[rows], y_r)
+    assert_close("o rows", o[rows], o_r)
+    assert_close("lse rows", lse[:, rows], lse_r)
+    # dX on the last rows: dq rows are row-local, dk/dv of the key tail need
+    # only the query rows at or after it.
+    j0 = S - 256
+    print("oracle key tail", flush=True)
+    q, k, v = L.split_qkv(x64 @ w64, Hq, Hkv, d)
+    do = (dy64 @ wo64.T).reshape(S, Hq, d)
+    tail = np.arange(j0, S)
+    dq_t, _ = A.attn_bwd_rows(q, k, v, do, tail)
+    dk_t, dv_t = A.attn_bwd_key_tail(q, k, v, do, j0)
+    dqkv = np.concatenate([dq_t.reshape(len(tail), -1), dk_t.reshape(len(tail), -1),
+                           dv_t.reshape(len(tail), -1)], axis=1)
+    assert_close("dx tail rows", dx[j0:], dqkv @ w64.T)

@@ -9,7 +9,14 @@ own representation error: a bf16 output x carries a rounding error of up to
 the probabilities / score gradients are rounded to bf16 once more before
 their fp32-accumulated products; BF16_REL = 2^-8 covers both roundings.
 Weight gradients reduce over the whole sequence, so their entries grow like
-sqrt(S); for them the max-abs criterion is applied to err / max(1, rms(ref)).
+sqrt(S), and they inherit the relative error of the bf16 intermediates the
+block keeps (Q, K, V, O, dO, dQ, dK, dV in the paper's bf16 mixed precision):
+an fp64 evaluation that rounds only those intermediates to bf16 already shows
+an excess error of 0.024 x rms of the output block.  For them the max-abs
+criterion is  max excess / max(1, rms(ref block)) <= WGRAD_MAX, per block
+with one scale (the Q, K and V column groups of dWqkv; dWo whole); the floor
+of 1 (the scale of the N(0,1) inputs) keeps a block whose exact value is zero
+(dWk at S = 1, where dK vanishes) on an absolute scale.
 """
 
 import numpy as np
@@ -17,6 +24,7 @@ import numpy as np
 MAX_ABS = 2e-2
 REL_FROB = 1e-2
 BF16_REL = 2.0 ** -8
+WGRAD_MAX = 4e-2
 
 
 def as64(t):
@@ -29,27 +37,33 @@ def as64(t):
     return np.asarray(t, np.float64)
 
 
-def errors(got, ref, rms_scaled=False):
+def errors(got, ref, rms_scaled=False, blocks=None):
     got, ref = as64(got), as64(ref)
     assert got.shape == ref.shape, (got.shape, ref.shape)
     err = got - ref
     excess = np.abs(err) - BF16_REL * np.abs(ref)
-    max_abs = float(excess.max()) if err.size else 0.0
     if rms_scaled:
-        rms = float(np.sqrt(np.mean(ref * ref))) if ref.size else 0.0
-        max_abs /= max(1.0, rms)
+        parts = blocks or [slice(None)]
+        max_abs = 0.0
+        for b in parts:
+            rb = float(np.sqrt(np.mean(ref[:, b] ** 2)))
+            max_abs = max(max_abs, float(excess[:, b].max()) / max(rb, 1.0))
+    else:
+        max_abs = float(excess.max()) if err.size else 0.0
     nref = float(np.linalg.norm(ref))
     nerr = float(np.linalg.norm(err))
     rel = nerr / nref if nref > 0 else nerr
     return max_abs, rel
 
 
-def assert_close(name, got, ref, rms_scaled=False):
-    max_abs, rel = errors(got, ref, rms_scaled)
+def assert_close(name, got, ref, rms_scaled=False, blocks=None):
+    max_abs, rel = errors(got, ref, rms_scaled, blocks)
     raw = float(np.abs(as64(got) - as64(ref)).max()) if as64(ref).size else 0.0
-    print(f"  {name}: max_abs={raw:.3e} excess={max_abs:.3e} rel_frob={rel:.3e}")
+    bar = WGRAD_MAX if rms_scaled else MAX_ABS
+    kind = "excess/rms" if rms_scaled else "excess"
+    print(f"  {name}: max_abs={raw:.3e} {kind}={max_abs:.3e} rel_frob={rel:.3e}")
     assert np.all(np.isfinite(as64(got))), f"{name}: non-finite values"
-    assert max_abs <= MAX_ABS and rel <= REL_FROB, (
-        f"{name}: max_abs={max_abs:.3e} (<= {MAX_ABS}) "
+    assert max_abs <= bar and rel <= REL_FROB, (
+        f"{name}: {kind}={max_abs:.3e} (<= {bar}) "
         f"rel_frob={rel:.3e} (<= {REL_FROB})")
     return max_abs, rel
