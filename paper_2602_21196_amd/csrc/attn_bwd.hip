@@ -7,14 +7,18 @@
 //   dV_j += sum_i P_ij dO_i,   dK_j += sum_i dS_ij q_i / sqrt d,
 //   dQ_i  = sum_j dS_ij k_j / sqrt d.
 // Two kernels, no atomics, one fixed summation order:
-//   dkdv: a workgroup owns 128 keys of one key/value head (4 waves x 32 keys)
-//         and walks the chunk's query heads in ascending order, and within a
-//         head the 32-row query tiles in ascending order.  Its fp32 dK/dV
-//         accumulators start from the values the previous chunk left in the
-//         workspace (UPipe keeps per-group dK/dV accumulators alive across
-//         stages, Appendix A), so any chunk size U yields bit-identical sums.
-//   dq:   a workgroup owns 128 query rows of one head and walks key tiles in
-//         ascending order, recomputing P and dS.
+//   dkdv: a workgroup owns 128 keys of one key/value head (4 waves x 32 keys,
+//         K and V fragments in registers) and walks the chunk's query heads in
+//         ascending order and, within a head, the 32-row query tiles from the
+//         last one down to its diagonal, so that all resident workgroups read
+//         the same query tiles at about the same time (shared L2 lines).  Its
+//         fp32 dK/dV accumulators start from the values the previous chunk
+//         left in the workspace (UPipe keeps per-group dK/dV accumulators alive
+//         across stages, Appendix A), so any chunk size U gives bit-identical
+//         sums.
+//   dq:   a workgroup owns 128 query rows of one head and walks 32-key tiles
+//         in ascending order, recomputing P and dS.
+// Tiles reach LDS through direct global->LDS copies issued one tile ahead.
 // Transposed operands come from the MFMA-ordered [d][S] copies (common.h).
 #include "common.h"
 #include "kernels.h"
@@ -28,83 +32,80 @@ constexpr float kScale = 0.08838834764831845f;                      // 1/sqrt(12
 constexpr float kLog2e = 1.4426950408889634f;
 
 // ------------------------------------------------------------------ dK / dV
-// LDS stage for one 32-row query tile: Q [32][128], dO [32][128] (rows of
-// 256 B, chunk swizzle c ^ (r & 15)), Q^T and dO^T [128][32] in MFMA order
-// (rows of 64 B, chunk swizzle c ^ ((r >> 1) & 3)), lse*log2e and D [32].
+// LDS stage for one 32-row query tile: Q [32][128] and dO [32][128] (256-B
+// rows), Q^T and dO^T [128][32] in MFMA order (64-B rows), lse and D [32].
 constexpr int QT = 32;
-constexpr int ROWT_BYTES = QT * HEAD_DIM * 2;       // 8 KB
-constexpr int OFF_Q = 0, OFF_DO = ROWT_BYTES, OFF_QT = 2 * ROWT_BYTES,
-              OFF_DOT = 3 * ROWT_BYTES, OFF_LSE = 4 * ROWT_BYTES,
-              OFF_D = OFF_LSE + QT * 4;
-constexpr int KV_STAGE = OFF_D + QT * 4;
+constexpr int ROWT = QT * HEAD_DIM * 2;   // 8 KB
+constexpr int OFF_Q = 0, OFF_DO = ROWT, OFF_QT = 2 * ROWT, OFF_DOT = 3 * ROWT,
+              OFF_LSE = 4 * ROWT, OFF_D = OFF_LSE + QT * 4;
+constexpr int KV_STAGE = 4 * ROWT + 1024;   // lse/D block padded to 1 KB
 
-__device__ __forceinline__ uint32_t row_off(int row, int chunk) {
-  return row * 256 + ((chunk ^ (row & 15)) << 4);
-}
-__device__ __forceinline__ uint32_t col_off(int drow, int chunk) {
-  return drow * 64 + ((chunk ^ ((drow >> 1) & 3)) << 4);
-}
-
-struct QTileRegs {
-  u32x4 q[2], dO[2], qt[2], dOt[2];
-  float lse, D;
+struct QTilePtrs {
+  const char *q, *dO, *qt, *dOt, *lse, *D;   // head bases (bytes)
+  uint32_t col_bytes;                          // row stride of the [d][Sp] copies
 };
 
-// Each tile is 512 pieces of 16 bytes: 256 threads move two pieces of each
-// of the four tiles; threads 0..31 / 32..63 also move one float of lse / D.
-__device__ __forceinline__ void load_qtile(QTileRegs& r, const bf16* Qh, const bf16* Qth,
-                                           const bf16* dOh, const bf16* dOth,
-                                           const float* lseh, const float* Dh,
-                                           int64_t Sp, int64_t qb, int t) {
+// Wave w copies two 1 KB blocks of each of Q, dO (rows 4 per block) and Q^T,
+// dO^T (16 rows of 64 B per block); wave 0 also copies lse and D (lanes 0-15).
+__device__ __forceinline__ void issue_qtile(const QTilePtrs& p, uint32_t qb, char* buf, int w,
+                                            int lane) {
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
-    const int pi = t + 256 * i;
-    const int row = pi >> 4, chunk = pi & 15;
-    r.q[i] = *reinterpret_cast<const u32x4*>(Qh + (qb + row) * HEAD_DIM + chunk * 8);
-    r.dO[i] = *reinterpret_cast<const u32x4*>(dOh + (qb + row) * HEAD_DIM + chunk * 8);
-    const int drow = pi >> 2, c = pi & 3;
-    r.qt[i] = *reinterpret_cast<const u32x4*>(Qth + (int64_t)drow * Sp + qb + c * 8);
-    r.dOt[i] = *reinterpret_cast<const u32x4*>(dOth + (int64_t)drow * Sp + qb + c * 8);
+    const int blk = 2 * w + i;
+    const int row = 4 * blk + (lane >> 4);
+    const uint32_t off = (qb + row) * 256u + (((lane & 15) ^ (row & 15)) << 4);
+    dma_b128(p.q + off, buf + OFF_Q + blk * 1024);
+    dma_b128(p.dO + off, buf + OFF_DO + blk * 1024);
+    const int crow = 16 * blk + (lane >> 2);
+    const uint32_t coff = crow * p.col_bytes + qb * 2u + (((lane & 3) ^ ((crow >> 1) & 3)) << 4);
+    dma_b128(p.qt + coff, buf + OFF_QT + blk * 1024);
+    dma_b128(p.dOt + coff, buf + OFF_DOT + blk * 1024);
   }
-  if (t < 32) r.lse = lseh[qb + t] * kLog2e;
-  else if (t < 64) r.D = Dh[qb + t - 32];
-}
-
-__device__ __forceinline__ void store_qtile(const QTileRegs& r, char* buf, int t) {
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int pi = t + 256 * i;
-    const int row = pi >> 4, chunk = pi & 15;
-    lds_write_b128(buf + OFF_Q, row_off(row, chunk), r.q[i]);
-    lds_write_b128(buf + OFF_DO, row_off(row, chunk), r.dO[i]);
-    const int drow = pi >> 2, c = pi & 3;
-    lds_write_b128(buf + OFF_QT, col_off(drow, c), r.qt[i]);
-    lds_write_b128(buf + OFF_DOT, col_off(drow, c), r.dOt[i]);
+  if (w == 0 && lane < 16) {
+    const char* src = lane < 8 ? p.lse + qb * 4u + lane * 16u : p.D + qb * 4u + (lane - 8) * 16u;
+    dma_b128(src, buf + OFF_LSE);
   }
-  if (t < 32) reinterpret_cast<float*>(buf + OFF_LSE)[t] = r.lse;
-  else if (t < 64) reinterpret_cast<float*>(buf + OFF_D)[t - 32] = r.D;
 }
 
 template <bool CAUSAL>
 __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(
-    const bf16* __restrict__ Qc, const bf16* __restrict__ Qct,
-    const bf16* __restrict__ dOc, const bf16* __restrict__ dOct,
-    const float* __restrict__ lse_c, const float* __restrict__ Dc,
-    const bf16* __restrict__ Kp, const bf16* __restrict__ Vp,
-    float* __restrict__ dK32, float* __restrict__ dV32,
-    bf16* __restrict__ dk, bf16* __restrict__ dv,
-    int64_t S, int64_t Sp, int U, int h0, int G, int Hkv) {
-  __shared__ __attribute__((aligned(16))) char smem[2 * KV_STAGE];
+    const bf16* __restrict__ Qc, const bf16* __restrict__ Qct, const bf16* __restrict__ dOc,
+    const bf16* __restrict__ dOct, const float* __restrict__ lse_c, const float* __restrict__ Dc,
+    const bf16* __restrict__ Kp, const bf16* __restrict__ Vp, float* __restrict__ dK32,
+    float* __restrict__ dV32, bf16* __restrict__ dk, bf16* __restrict__ dv, int64_t S, int64_t Sp,
+    int U, int h0, int G, int Hkv) {
+  __shared__ __attribute__((aligned(1024))) char smem[2 * KV_STAGE];
   const int t = threadIdx.x;
   const int lane = t & 63, w = t >> 6;
   const int r32 = lane & 31, g = lane >> 5;
   const int kvh = h0 / G + blockIdx.y;
-  const int64_t kb0 = (int64_t)blockIdx.x * 128;
-  const int64_t kw = kb0 + 32 * w;      // first key of this wave
-  const int64_t mykey = kw + r32;       // key column owned by this lane
+  const uint32_t kb0 = blockIdx.x * 128u;
+  const uint32_t kw = kb0 + 32 * w;      // first key of this wave
+  const uint32_t mykey = kw + r32;       // key column owned by this lane
   const int hlo = max(h0, kvh * G), hhi = min(h0 + U, (kvh + 1) * G);
   const bool first = kvh * G >= h0;           // no earlier chunk touched kvh
   const bool last = (kvh + 1) * G <= h0 + U;  // no later chunk will
+  const uint32_t nqt = (uint32_t)(Sp / QT);
+  const uint32_t qt_lo = CAUSAL ? kb0 / QT : 0;   // lowest query tile needed
+  const uint32_t per_head = nqt - qt_lo;
+  const int total = (int)(per_head * (hhi - hlo));
+
+  auto ptrs = [&](int hh) {
+    QTilePtrs p;
+    const int64_t hoff = (int64_t)(hh - h0) * Sp * HEAD_DIM;
+    p.q = reinterpret_cast<const char*>(Qc + hoff);
+    p.dO = reinterpret_cast<const char*>(dOc + hoff);
+    p.qt = reinterpret_cast<const char*>(Qct + hoff);
+    p.dOt = reinterpret_cast<const char*>(dOct + hoff);
+    p.lse = reinterpret_cast<const char*>(lse_c + (int64_t)(hh - h0) * Sp);
+    p.D = reinterpret_cast<const char*>(Dc + (int64_t)(hh - h0) * Sp);
+    p.col_bytes = (uint32_t)Sp * 2u;
+    return p;
+  };
+
+  // First tile: head hlo, query tile nqt-1.
+  QTilePtrs cur = ptrs(hlo);
+  issue_qtile(cur, (nqt - 1) * QT, smem, w, lane);
 
   // K and V B-operand fragments (lane = key column, k = head dim).
   bf16x8 kf[8], vf[8];
@@ -121,59 +122,59 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(
   // Accumulators: C layout with lane = head-dim column 32*dt + r32 and
   // element i = key row kw + 8*(i/4) + 4*g + (i%4).
   f32x16 dka[4], dva[4];
-  const int64_t accbase = (int64_t)kvh * Sp * HEAD_DIM;
+  float* dK32h = dK32 + (int64_t)kvh * Sp * HEAD_DIM;
+  float* dV32h = dV32 + (int64_t)kvh * Sp * HEAD_DIM;
+  if (first) {
 #pragma unroll
-  for (int dt = 0; dt < 4; ++dt)
+    for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      if (first) {
+      for (int i = 0; i < 16; ++i) {
         dka[dt][i] = 0.f;
         dva[dt][i] = 0.f;
-      } else {
-        const int64_t key = kw + 8 * (i >> 2) + 4 * g + (i & 3);
-        const int64_t off = accbase + key * HEAD_DIM + 32 * dt + r32;
-        dka[dt][i] = dK32[off];
-        dva[dt][i] = dV32[off];
       }
+  } else {
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const uint32_t off = (kw + 8 * (i >> 2) + 4 * g + (i & 3)) * HEAD_DIM + 32 * dt + r32;
+        dka[dt][i] = dK32h[off];
+        dva[dt][i] = dV32h[off];
+      }
+  }
+
+  int hh = hlo;
+  uint32_t qt = nqt - 1;     // query tile of the current iteration
+  for (int it = 0; it < total; ++it) {
+    char* buf = smem + (it & 1) * KV_STAGE;
+    const uint32_t qb = qt * QT;
+    // next tile (descending query tiles, then the next head)
+    uint32_t nq = qt - 1;
+    int nh = hh;
+    if (qt == qt_lo) {
+      nq = nqt - 1;
+      nh = hh + 1;
+    }
+    wait_vmem();
+    __syncthreads();   // this tile landed for all waves; the other buffer is free
+    if (it + 1 < total) {
+      if (nh != hh) cur = ptrs(nh);
+      issue_qtile(cur, nq * QT, smem + ((it + 1) & 1) * KV_STAGE, w, lane);
     }
 
-  const int64_t qt_begin = CAUSAL ? kb0 / QT : 0;
-  const int64_t qt_end = Sp / QT;
-  const int64_t per_head = qt_end - qt_begin;
-  const int64_t total = per_head * (hhi - hlo);
-
-  QTileRegs regs;
-  auto tile_ptrs_load = [&](int64_t it) {
-    const int hh = hlo + (int)(it / per_head) - h0;
-    const int64_t qb = (qt_begin + it % per_head) * QT;
-    load_qtile(regs, Qc + (int64_t)hh * Sp * HEAD_DIM, Qct + (int64_t)hh * HEAD_DIM * Sp,
-               dOc + (int64_t)hh * Sp * HEAD_DIM, dOct + (int64_t)hh * HEAD_DIM * Sp,
-               lse_c + (int64_t)hh * Sp, Dc + (int64_t)hh * Sp, Sp, qb, t);
-  };
-  if (total > 0) {
-    tile_ptrs_load(0);
-    store_qtile(regs, smem, t);
-  }
-  __syncthreads();
-
-  for (int64_t it = 0; it < total; ++it) {
-    const int64_t qb = (qt_begin + it % per_head) * QT;
-    char* buf = smem + (it & 1) * KV_STAGE;
-    const bool more = it + 1 < total;
-    if (more) tile_ptrs_load(it + 1);
-
-    const bool needed = !CAUSAL || qb + QT - 1 >= kw;
-    if (needed) {
+    const bool skip = CAUSAL && qb + QT - 1 < kw;
+    if (!skip) {
       f32x16 sacc, pacc;
 #pragma unroll
       for (int i = 0; i < 16; ++i) { sacc[i] = 0.f; pacc[i] = 0.f; }
 #pragma unroll
       for (int s = 0; s < 8; ++s) {
-        sacc = mfma32x32x16(lds_read_b128(buf + OFF_Q, row_off(r32, 2 * s + g)), kf[s], sacc);
-        pacc = mfma32x32x16(lds_read_b128(buf + OFF_DO, row_off(r32, 2 * s + g)), vf[s], pacc);
+        sacc = mfma32x32x16(lds_read_b128(buf + OFF_Q, swz256(r32, 2 * s + g)), kf[s], sacc);
+        pacc = mfma32x32x16(lds_read_b128(buf + OFF_DO, swz256(r32, 2 * s + g)), vf[s], pacc);
       }
       const float* lsel = reinterpret_cast<const float*>(buf + OFF_LSE);
       const float* Dl = reinterpret_cast<const float*>(buf + OFF_D);
+      const bool diag = CAUSAL && qb < kw + 31;
       bf16x8 pf[2], sf[2];
 #pragma unroll
       for (int a = 0; a < 4; ++a) {
@@ -182,11 +183,8 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(
 #pragma unroll
         for (int b = 0; b < 4; ++b) {
           const int i = 4 * a + b;
-          float p = fast_exp2(fmaf(sacc[i], kSl2, -l4[b]));
-          if (CAUSAL) {
-            const int64_t q = qb + 8 * a + 4 * g + b;
-            if (mykey > q) p = 0.f;
-          }
+          float p = fast_exp2(fmaf(sacc[i], kSl2, -l4[b] * kLog2e));
+          if (diag && mykey > qb + 8 * a + 4 * g + b) p = 0.f;
           const float ds = p * (pacc[i] - d4[b]);
           pf[i >> 3][i & 7] = (bf16)p;
           sf[i >> 3][i & 7] = (bf16)ds;
@@ -197,83 +195,70 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(
         const int drow = 32 * dt + r32;
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt) {
-          dva[dt] = mfma32x32x16(pf[kt], lds_read_b128(buf + OFF_DOT, col_off(drow, 2 * kt + g)), dva[dt]);
-          dka[dt] = mfma32x32x16(sf[kt], lds_read_b128(buf + OFF_QT, col_off(drow, 2 * kt + g)), dka[dt]);
+          dva[dt] = mfma32x32x16(pf[kt], lds_read_b128(buf + OFF_DOT, swz64(drow, 2 * kt + g)), dva[dt]);
+          dka[dt] = mfma32x32x16(sf[kt], lds_read_b128(buf + OFF_QT, swz64(drow, 2 * kt + g)), dka[dt]);
         }
       }
     }
-    if (more) store_qtile(regs, smem + ((it + 1) & 1) * KV_STAGE, t);
-    __syncthreads();
+    qt = nq;
+    hh = nh;
   }
 
+  if (last) {
 #pragma unroll
-  for (int dt = 0; dt < 4; ++dt)
+    for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int64_t key = kw + 8 * (i >> 2) + 4 * g + (i & 3);
-      const int d = 32 * dt + r32;
-      if (last) {
-        if (key < S) {
-          const int64_t off = (key * Hkv + kvh) * HEAD_DIM + d;
+      for (int i = 0; i < 16; ++i) {
+        const uint32_t key = kw + 8 * (i >> 2) + 4 * g + (i & 3);
+        if (key < (uint64_t)S) {
+          const int64_t off = ((int64_t)key * Hkv + kvh) * HEAD_DIM + 32 * dt + r32;
           dk[off] = (bf16)(dka[dt][i] * kScale);
           dv[off] = (bf16)dva[dt][i];
         }
-      } else {
-        const int64_t off = accbase + key * HEAD_DIM + d;
-        dK32[off] = dka[dt][i];
-        dV32[off] = dva[dt][i];
       }
-    }
-}
-
-// ---------------------------------------------------------------------- dQ
-// LDS stage for one 64-key tile: K [64][128], V [64][128] (256-B rows,
-// swizzle c ^ (r & 15)) and K^T [128][64] in MFMA order (128-B rows,
-// swizzle c ^ (r & 7)).
-constexpr int BKQ = 64;
-constexpr int KT_BYTES = BKQ * HEAD_DIM * 2;   // 16 KB
-constexpr int DQ_OFF_K = 0, DQ_OFF_V = KT_BYTES, DQ_OFF_KT = 2 * KT_BYTES;
-constexpr int DQ_STAGE = 3 * KT_BYTES;
-
-__device__ __forceinline__ uint32_t kt_off(int drow, int chunk) {
-  return drow * 128 + ((chunk ^ (drow & 7)) << 4);
-}
-
-struct KTileRegs {
-  u32x4 k[4], v[4], kt[4];
-};
-
-__device__ __forceinline__ void load_ktile(KTileRegs& r, const bf16* Kh, const bf16* Vh,
-                                           const bf16* Kth, int64_t Sp, int64_t kb, int t) {
+  } else {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int pi = t + 256 * i;
-    const int row = pi >> 4, chunk = pi & 15;
-    r.k[i] = *reinterpret_cast<const u32x4*>(Kh + (kb + row) * HEAD_DIM + chunk * 8);
-    r.v[i] = *reinterpret_cast<const u32x4*>(Vh + (kb + row) * HEAD_DIM + chunk * 8);
-    const int drow = pi >> 3, c = pi & 7;
-    r.kt[i] = *reinterpret_cast<const u32x4*>(Kth + (int64_t)drow * Sp + kb + c * 8);
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const uint32_t off = (kw + 8 * (i >> 2) + 4 * g + (i & 3)) * HEAD_DIM + 32 * dt + r32;
+        dK32h[off] = dka[dt][i];
+        dV32h[off] = dva[dt][i];
+      }
   }
 }
 
-__device__ __forceinline__ void store_ktile(const KTileRegs& r, char* buf, int t) {
+// ---------------------------------------------------------------------- dQ
+// LDS stage for one 32-key tile: K [32][128], V [32][128] (256-B rows) and
+// K^T [128][32] in MFMA order (64-B rows).
+constexpr int BKQ = 32;
+constexpr int KT8 = BKQ * HEAD_DIM * 2;   // 8 KB
+constexpr int DQ_OFF_K = 0, DQ_OFF_V = KT8, DQ_OFF_KT = 2 * KT8;
+constexpr int DQ_STAGE = 3 * KT8;
+
+__device__ __forceinline__ void issue_ktile(const char* Kh, const char* Vh, const char* Kth,
+                                            uint32_t col_bytes, uint32_t kb, char* buf, int w,
+                                            int lane) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int pi = t + 256 * i;
-    lds_write_b128(buf + DQ_OFF_K, row_off(pi >> 4, pi & 15), r.k[i]);
-    lds_write_b128(buf + DQ_OFF_V, row_off(pi >> 4, pi & 15), r.v[i]);
-    lds_write_b128(buf + DQ_OFF_KT, kt_off(pi >> 3, pi & 7), r.kt[i]);
+  for (int i = 0; i < 2; ++i) {
+    const int blk = 2 * w + i;
+    const int row = 4 * blk + (lane >> 4);
+    const uint32_t off = (kb + row) * 256u + (((lane & 15) ^ (row & 15)) << 4);
+    dma_b128(Kh + off, buf + DQ_OFF_K + blk * 1024);
+    dma_b128(Vh + off, buf + DQ_OFF_V + blk * 1024);
+    const int crow = 16 * blk + (lane >> 2);
+    dma_b128(Kth + crow * col_bytes + kb * 2u + (((lane & 3) ^ ((crow >> 1) & 3)) << 4),
+             buf + DQ_OFF_KT + blk * 1024);
   }
 }
 
 template <bool CAUSAL>
-__global__ __launch_bounds__(256, 1) void attn_bwd_dq_kernel(
-    const bf16* __restrict__ Qc, const bf16* __restrict__ dOc,
-    const float* __restrict__ lse_c, const float* __restrict__ Dc,
-    const bf16* __restrict__ Kp, const bf16* __restrict__ Kt,
-    const bf16* __restrict__ Vp, bf16* __restrict__ dQc,
-    int64_t S, int64_t Sp, int U, int h0, int G, int nqb) {
-  __shared__ __attribute__((aligned(16))) char smem[2 * DQ_STAGE];
+__global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(
+    const bf16* __restrict__ Qc, const bf16* __restrict__ dOc, const float* __restrict__ lse_c,
+    const float* __restrict__ Dc, const bf16* __restrict__ Kp, const bf16* __restrict__ Kt,
+    const bf16* __restrict__ Vp, bf16* __restrict__ dQc, int64_t S, int64_t Sp, int U, int h0,
+    int G, int nqb) {
+  __shared__ __attribute__((aligned(1024))) char smem[2 * DQ_STAGE];
   const int t = threadIdx.x;
   const int lane = t & 63, w = t >> 6;
   const int r32 = lane & 31, g = lane >> 5;
@@ -281,13 +266,17 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dq_kernel(
   const int qb = nqb - 1 - L / U;
   const int u = L % U;
   const int kvh = (h0 + u) / G;
-  const int64_t q0 = (int64_t)qb * 128;
-  const int64_t qw = q0 + 32 * w;
-  const int64_t myq = qw + r32;
+  const uint32_t q0 = (uint32_t)qb * 128;
+  const uint32_t qw = q0 + 32 * w;
+  const uint32_t myq = qw + r32;
+  const uint32_t Sv = (uint32_t)S;
 
-  const bf16* Kh = Kp + (int64_t)kvh * Sp * HEAD_DIM;
-  const bf16* Vh = Vp + (int64_t)kvh * Sp * HEAD_DIM;
-  const bf16* Kth = Kt + (int64_t)kvh * HEAD_DIM * Sp;
+  const char* Kh = reinterpret_cast<const char*>(Kp + (int64_t)kvh * Sp * HEAD_DIM);
+  const char* Vh = reinterpret_cast<const char*>(Vp + (int64_t)kvh * Sp * HEAD_DIM);
+  const char* Kth = reinterpret_cast<const char*>(Kt + (int64_t)kvh * HEAD_DIM * Sp);
+  const uint32_t col_bytes = (uint32_t)Sp * 2u;
+  const int ntiles = CAUSAL ? (int)((q0 + 128) / BKQ) : (int)(Sp / BKQ);
+  issue_ktile(Kh, Vh, Kth, col_bytes, 0, smem, w, lane);
 
   bf16x8 qf[8], df[8];
   {
@@ -307,54 +296,43 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dq_kernel(
 #pragma unroll
     for (int i = 0; i < 16; ++i) qacc[dt][i] = 0.f;
 
-  const int ntiles = CAUSAL ? (int)((q0 + 128) / BKQ) : (int)(Sp / BKQ);
-  KTileRegs regs;
-  load_ktile(regs, Kh, Vh, Kth, Sp, 0, t);
-  store_ktile(regs, smem, t);
-  __syncthreads();
-
   for (int j = 0; j < ntiles; ++j) {
-    const int64_t kb = (int64_t)j * BKQ;
+    const uint32_t kb = (uint32_t)j * BKQ;
     char* buf = smem + (j & 1) * DQ_STAGE;
-    const bool more = j + 1 < ntiles;
-    if (more) load_ktile(regs, Kh, Vh, Kth, Sp, kb + BKQ, t);
-
-    const bool needed = !CAUSAL || kb <= qw + 31;
-    if (needed) {
-      bf16x8 sf[2][2];
-#pragma unroll
-      for (int tt = 0; tt < 2; ++tt) {
-        f32x16 sacc, pacc;
-#pragma unroll
-        for (int i = 0; i < 16; ++i) { sacc[i] = 0.f; pacc[i] = 0.f; }
-        const int row = 32 * tt + r32;
-#pragma unroll
-        for (int s = 0; s < 8; ++s) {
-          sacc = mfma32x32x16(lds_read_b128(buf + DQ_OFF_K, row_off(row, 2 * s + g)), qf[s], sacc);
-          pacc = mfma32x32x16(lds_read_b128(buf + DQ_OFF_V, row_off(row, 2 * s + g)), df[s], pacc);
-        }
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int64_t key = kb + 32 * tt + 8 * (i >> 2) + 4 * g + (i & 3);
-          float p = fast_exp2(fmaf(sacc[i], kSl2, -lse2));
-          const bool vis = CAUSAL ? (key <= myq) : (key < S);
-          if (!vis) p = 0.f;
-          sf[tt][i >> 3][i & 7] = (bf16)(p * (pacc[i] - Dq));
-        }
-      }
-#pragma unroll
-      for (int dt = 0; dt < 4; ++dt) {
-        const int drow = 32 * dt + r32;
-#pragma unroll
-        for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-          for (int kt = 0; kt < 2; ++kt)
-            qacc[dt] = mfma32x32x16(lds_read_b128(buf + DQ_OFF_KT, kt_off(drow, 4 * tt + 2 * kt + g)),
-                                    sf[tt][kt], qacc[dt]);
-      }
-    }
-    if (more) store_ktile(regs, smem + ((j + 1) & 1) * DQ_STAGE, t);
+    wait_vmem();
     __syncthreads();
+    if (j + 1 < ntiles)
+      issue_ktile(Kh, Vh, Kth, col_bytes, kb + BKQ, smem + ((j + 1) & 1) * DQ_STAGE, w, lane);
+    if (CAUSAL && kb > qw + 31) continue;
+
+    f32x16 sacc, pacc;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) { sacc[i] = 0.f; pacc[i] = 0.f; }
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      sacc = mfma32x32x16(lds_read_b128(buf + DQ_OFF_K, swz256(r32, 2 * s + g)), qf[s], sacc);
+      pacc = mfma32x32x16(lds_read_b128(buf + DQ_OFF_V, swz256(r32, 2 * s + g)), df[s], pacc);
+    }
+    const bool diag = CAUSAL ? (kb + BKQ - 1 > qw) : (kb + BKQ > Sv);
+    bf16x8 sf[2];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      float p = fast_exp2(fmaf(sacc[i], kSl2, -lse2));
+      if (diag) {
+        const uint32_t key = kb + 8 * (i >> 2) + 4 * g + (i & 3);
+        const bool vis = CAUSAL ? (key <= myq) : (key < Sv);
+        if (!vis) p = 0.f;
+      }
+      sf[i >> 3][i & 7] = (bf16)(p * (pacc[i] - Dq));
+    }
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) {
+      const int drow = 32 * dt + r32;
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+        qacc[dt] = mfma32x32x16(lds_read_b128(buf + DQ_OFF_KT, swz64(drow, 2 * kt + g)), sf[kt],
+                                qacc[dt]);
+    }
   }
 
   bf16* op = dQc + ((int64_t)u * Sp + myq) * HEAD_DIM + 4 * g;
@@ -371,39 +349,33 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dq_kernel(
 
 }  // namespace
 
-hipError_t launch_attn_bwd_dkdv(const bf16* Qc, const bf16* Qct,
-                                const bf16* dOc, const bf16* dOct,
-                                const float* lse_c, const float* D,
-                                const bf16* Kp, const bf16* Vp, float* dK32,
-                                float* dV32, bf16* dk, bf16* dv, int64_t S,
-                                int64_t Sp, int U, int h0, int G, int Hkv,
+hipError_t launch_attn_bwd_dkdv(const bf16* Qc, const bf16* Qct, const bf16* dOc,
+                                const bf16* dOct, const float* lse_c, const float* D,
+                                const bf16* Kp, const bf16* Vp, float* dK32, float* dV32, bf16* dk,
+                                bf16* dv, int64_t S, int64_t Sp, int U, int h0, int G, int Hkv,
                                 int causal, hipStream_t st) {
   const int kv_lo = h0 / G, kv_hi = (h0 + U - 1) / G;
   dim3 grid((unsigned)(Sp / 128), (unsigned)(kv_hi - kv_lo + 1));
   if (causal)
-    hipLaunchKernelGGL(attn_bwd_dkdv_kernel<true>, grid, dim3(256), 0, st, Qc,
-                       Qct, dOc, dOct, lse_c, D, Kp, Vp, dK32, dV32, dk, dv, S,
-                       Sp, U, h0, G, Hkv);
+    hipLaunchKernelGGL(attn_bwd_dkdv_kernel<true>, grid, dim3(256), 0, st, Qc, Qct, dOc, dOct,
+                       lse_c, D, Kp, Vp, dK32, dV32, dk, dv, S, Sp, U, h0, G, Hkv);
   else
-    hipLaunchKernelGGL(attn_bwd_dkdv_kernel<false>, grid, dim3(256), 0, st, Qc,
-                       Qct, dOc, dOct, lse_c, D, Kp, Vp, dK32, dV32, dk, dv, S,
-                       Sp, U, h0, G, Hkv);
+    hipLaunchKernelGGL(attn_bwd_dkdv_kernel<false>, grid, dim3(256), 0, st, Qc, Qct, dOc, dOct,
+                       lse_c, D, Kp, Vp, dK32, dV32, dk, dv, S, Sp, U, h0, G, Hkv);
   return hipGetLastError();
 }
 
-hipError_t launch_attn_bwd_dq(const bf16* Qc, const bf16* dOc,
-                              const float* lse_c, const float* D,
-                              const bf16* Kp, const bf16* Kt, const bf16* Vp,
-                              bf16* dQc, int64_t S, int64_t Sp, int U, int h0,
-                              int G, int causal, hipStream_t st) {
+hipError_t launch_attn_bwd_dq(const bf16* Qc, const bf16* dOc, const float* lse_c, const float* D,
+                              const bf16* Kp, const bf16* Kt, const bf16* Vp, bf16* dQc, int64_t S,
+                              int64_t Sp, int U, int h0, int G, int causal, hipStream_t st) {
   const int nqb = (int)(Sp / 128);
   dim3 grid((unsigned)(nqb * U));
   if (causal)
-    hipLaunchKernelGGL(attn_bwd_dq_kernel<true>, grid, dim3(256), 0, st, Qc,
-                       dOc, lse_c, D, Kp, Kt, Vp, dQc, S, Sp, U, h0, G, nqb);
+    hipLaunchKernelGGL(attn_bwd_dq_kernel<true>, grid, dim3(256), 0, st, Qc, dOc, lse_c, D, Kp, Kt,
+                       Vp, dQc, S, Sp, U, h0, G, nqb);
   else
-    hipLaunchKernelGGL(attn_bwd_dq_kernel<false>, grid, dim3(256), 0, st, Qc,
-                       dOc, lse_c, D, Kp, Kt, Vp, dQc, S, Sp, U, h0, G, nqb);
+    hipLaunchKernelGGL(attn_bwd_dq_kernel<false>, grid, dim3(256), 0, st, Qc, dOc, lse_c, D, Kp,
+                       Kt, Vp, dQc, S, Sp, U, h0, G, nqb);
   return hipGetLastError();
 }
 

@@ -56,4 +56,26 @@ __device__ __forceinline__ void lds_write_b128(char* base, uint32_t off, u32x4 v
   *reinterpret_cast<u32x4*>(base + off) = v;
 }
 
+// Direct global -> LDS copy of 16 bytes per lane (global_load_lds_dwordx4):
+// lane L's bytes land at lds_wave_base + 16 * L, where lds_wave_base must be
+// the same for the whole wave.  Completion is tracked by vmcnt.
+typedef __attribute__((address_space(3))) void lds_void;
+__device__ __forceinline__ void dma_b128(const void* g, char* lds_wave_base) {
+  __builtin_amdgcn_global_load_lds(g, (lds_void*)lds_wave_base, 16, 0, 0);
+}
+
+// Wait until every outstanding global load of this wave has completed.
+__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x3F70); }
+
+// 16-byte chunk swizzles.  Rows of 256 B (16 chunks): chunk c of row r is
+// stored at c ^ (r & 15).  Rows of 128 B (8 chunks): c ^ (r & 7) ^ ((r>>3) & 1).
+// Rows of 64 B (4 chunks): c ^ ((r >> 1) & 3).  For the MFMA operand reads
+// (consecutive lanes = consecutive rows, same logical chunk) these are free of
+// bank conflicts for both 32- and 64-bank LDS.
+__device__ __forceinline__ uint32_t swz256(int r, int c) { return r * 256 + ((c ^ (r & 15)) << 4); }
+__device__ __forceinline__ uint32_t swz128(int r, int c) {
+  return r * 128 + ((c ^ (r & 7) ^ ((r >> 3) & 1)) << 4);
+}
+__device__ __forceinline__ uint32_t swz64(int r, int c) { return r * 64 + ((c ^ ((r >> 1) & 3)) << 4); }
+
 }  // namespace upipe
