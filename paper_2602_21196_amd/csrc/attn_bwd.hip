@@ -9,8 +9,9 @@
 // Two kernels, no atomics, one fixed summation order:
 //   dkdv: a workgroup owns 128 keys of one key/value head (4 waves x 32 keys,
 //         K and V fragments in registers) and walks the chunk's query heads in
-//         ascending order and, within a head, the 32-row query tiles from the
-//         last one down to its diagonal, so that all resident workgroups read
+//         ascending order and, within a head, the 64-row query tiles from the
+//         last one down to its diagonal (the two 32-row halves of a tile in
+//         ascending order), so that all resident workgroups read
 //         the same query tiles at about the same time (shared L2 lines).  Its
 //         fp32 dK/dV accumulators start from the values the previous chunk
 //         left in the workspace (UPipe keeps per-group dK/dV accumulators alive
@@ -29,13 +30,14 @@ namespace {
 
 constexpr float kSl2 = 1.4426950408889634f * 0.08838834764831845f;  // log2(e)/sqrt(128)
 constexpr float kScale = 0.08838834764831845f;                      // 1/sqrt(128)
-constexpr float kLog2e = 1.4426950408889634f;
 
 // ------------------------------------------------------------------ dK / dV
-// LDS stage for one 32-row query tile: Q [32][128] and dO [32][128] (256-B
-// rows), Q^T and dO^T [128][32] in MFMA order (64-B rows), lse and D [32].
-constexpr int QT = 32;
-constexpr int ROWT = QT * HEAD_DIM * 2;   // 8 KB
+// LDS stage for one 64-row query tile (two 32-row subtiles): Q [64][128] and
+// dO [64][128] (256-B rows), Q^T and dO^T [128][64] in MFMA order (128-B
+// rows), lse and D [64].  Two subtiles per stage let one subtile's softmax
+// gradient (VALU) overlap the other's products (MFMA) within a wave.
+constexpr int QT = 64;
+constexpr int ROWT = QT * HEAD_DIM * 2;   // 16 KB
 constexpr int OFF_Q = 0, OFF_DO = ROWT, OFF_QT = 2 * ROWT, OFF_DOT = 3 * ROWT,
               OFF_LSE = 4 * ROWT, OFF_D = OFF_LSE + QT * 4;
 constexpr int KV_STAGE = 4 * ROWT + 1024;   // lse/D block padded to 1 KB
@@ -45,25 +47,68 @@ struct QTilePtrs {
   uint32_t col_bytes;                          // row stride of the [d][Sp] copies
 };
 
-// Wave w copies two 1 KB blocks of each of Q, dO (rows 4 per block) and Q^T,
-// dO^T (16 rows of 64 B per block); wave 0 also copies lse and D (lanes 0-15).
+// Wave w copies four 1 KB blocks of each of Q, dO (4 rows of 256 B per block)
+// and Q^T, dO^T (8 rows of 128 B per block); wave 0 also copies lse and D.
 __device__ __forceinline__ void issue_qtile(const QTilePtrs& p, uint32_t qb, char* buf, int w,
                                             int lane) {
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int blk = 2 * w + i;
+  for (int i = 0; i < 4; ++i) {
+    const int blk = 4 * w + i;
     const int row = 4 * blk + (lane >> 4);
     const uint32_t off = (qb + row) * 256u + (((lane & 15) ^ (row & 15)) << 4);
     dma_b128(p.q + off, buf + OFF_Q + blk * 1024);
     dma_b128(p.dO + off, buf + OFF_DO + blk * 1024);
-    const int crow = 16 * blk + (lane >> 2);
-    const uint32_t coff = crow * p.col_bytes + qb * 2u + (((lane & 3) ^ ((crow >> 1) & 3)) << 4);
+    const int crow = 8 * blk + (lane >> 3);
+    const uint32_t coff = crow * p.col_bytes + qb * 2u +
+                          (((lane & 7) ^ (crow & 7) ^ ((crow >> 3) & 1)) << 4);
     dma_b128(p.qt + coff, buf + OFF_QT + blk * 1024);
     dma_b128(p.dOt + coff, buf + OFF_DOT + blk * 1024);
   }
-  if (w == 0 && lane < 16) {
-    const char* src = lane < 8 ? p.lse + qb * 4u + lane * 16u : p.D + qb * 4u + (lane - 8) * 16u;
+  if (w == 0 && lane < 32) {
+    const char* src = lane < 16 ? p.lse + qb * 4u + lane * 16u : p.D + qb * 4u + (lane - 16) * 16u;
     dma_b128(src, buf + OFF_LSE);
+  }
+}
+
+// One 32-row query subtile: rows qs..qs+31 at offset `sub` (0 or 32) in the
+// stage.  Returns the bf16 P and dS fragments for the dV / dK products.
+template <bool CAUSAL>
+__device__ __forceinline__ void subtile_scores(const char* buf, int sub, uint32_t qs,
+                                               uint32_t mykey, bool diag, int r32, int g,
+                                               const bf16x8 (&kf)[8], const bf16x8 (&vf)[8],
+                                               bf16x8 (&pf)[2], bf16x8 (&sf)[2]) {
+  f32x16 sacc, pacc;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) { sacc[i] = 0.f; pacc[i] = 0.f; }
+  const int row = sub + r32;
+#pragma unroll
+  for (int s = 0; s < 8; ++s) {
+    sacc = mfma32x32x16(lds_read_b128(buf + OFF_Q, swz256(row, 2 * s + g)), kf[s], sacc);
+    pacc = mfma32x32x16(lds_read_b128(buf + OFF_DO, swz256(row, 2 * s + g)), vf[s], pacc);
+  }
+  const float* lsel = reinterpret_cast<const float*>(buf + OFF_LSE) + sub;
+  const float* Dl = reinterpret_cast<const float*>(buf + OFF_D) + sub;
+  float p[16];
+#pragma unroll
+  for (int a = 0; a < 4; ++a) {
+    const f32x4 l4 = *reinterpret_cast<const f32x4*>(lsel + 8 * a + 4 * g);
+#pragma unroll
+    for (int b = 0; b < 4; ++b) p[4 * a + b] = fast_exp2(fmaf(sacc[4 * a + b], kSl2, -l4[b]));
+  }
+  if (CAUSAL && diag) {   // wave-uniform: only tiles that cross the diagonal
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      if (mykey > qs + 8 * (i >> 2) + 4 * g + (i & 3)) p[i] = 0.f;
+  }
+#pragma unroll
+  for (int a = 0; a < 4; ++a) {
+    const f32x4 d4 = *reinterpret_cast<const f32x4*>(Dl + 8 * a + 4 * g);
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int i = 4 * a + b;
+      pf[i >> 3][i & 7] = (bf16)p[i];
+      sf[i >> 3][i & 7] = (bf16)(p[i] * (pacc[i] - d4[b]));
+    }
   }
 }
 
@@ -162,32 +207,23 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(
       issue_qtile(cur, nq * QT, smem + ((it + 1) & 1) * KV_STAGE, w, lane);
     }
 
-    const bool skip = CAUSAL && qb + QT - 1 < kw;
-    if (!skip) {
-      f32x16 sacc, pacc;
+    // Subtile 1 (rows qb+32..63) is needed whenever subtile 0 is.
+    const bool need0 = !CAUSAL || qb + 31 >= kw;
+    const bool need1 = !CAUSAL || qb + 63 >= kw;
+    if (need1) {
+      bf16x8 pf1[2], sf1[2];
+      subtile_scores<CAUSAL>(buf, 32, qb + 32, mykey, qb + 32 < kw + 31, r32, g, kf, vf, pf1, sf1);
+      if (need0) {
+        bf16x8 pf0[2], sf0[2];
+        subtile_scores<CAUSAL>(buf, 0, qb, mykey, qb < kw + 31, r32, g, kf, vf, pf0, sf0);
 #pragma unroll
-      for (int i = 0; i < 16; ++i) { sacc[i] = 0.f; pacc[i] = 0.f; }
+        for (int dt = 0; dt < 4; ++dt) {
+          const int drow = 32 * dt + r32;
 #pragma unroll
-      for (int s = 0; s < 8; ++s) {
-        sacc = mfma32x32x16(lds_read_b128(buf + OFF_Q, swz256(r32, 2 * s + g)), kf[s], sacc);
-        pacc = mfma32x32x16(lds_read_b128(buf + OFF_DO, swz256(r32, 2 * s + g)), vf[s], pacc);
-      }
-      const float* lsel = reinterpret_cast<const float*>(buf + OFF_LSE);
-      const float* Dl = reinterpret_cast<const float*>(buf + OFF_D);
-      const bool diag = CAUSAL && qb < kw + 31;
-      bf16x8 pf[2], sf[2];
-#pragma unroll
-      for (int a = 0; a < 4; ++a) {
-        const f32x4 l4 = *reinterpret_cast<const f32x4*>(lsel + 8 * a + 4 * g);
-        const f32x4 d4 = *reinterpret_cast<const f32x4*>(Dl + 8 * a + 4 * g);
-#pragma unroll
-        for (int b = 0; b < 4; ++b) {
-          const int i = 4 * a + b;
-          float p = fast_exp2(fmaf(sacc[i], kSl2, -l4[b] * kLog2e));
-          if (diag && mykey > qb + 8 * a + 4 * g + b) p = 0.f;
-          const float ds = p * (pacc[i] - d4[b]);
-          pf[i >> 3][i & 7] = (bf16)p;
-          sf[i >> 3][i & 7] = (bf16)ds;
+          for (int kt = 0; kt < 2; ++kt) {
+            dva[dt] = mfma32x32x16(pf0[kt], lds_read_b128(buf + OFF_DOT, swz128(drow, 2 * kt + g)), dva[dt]);
+            dka[dt] = mfma32x32x16(sf0[kt], lds_read_b128(buf + OFF_QT, swz128(drow, 2 * kt + g)), dka[dt]);
+          }
         }
       }
 #pragma unroll
@@ -195,8 +231,8 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(
         const int drow = 32 * dt + r32;
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt) {
-          dva[dt] = mfma32x32x16(pf[kt], lds_read_b128(buf + OFF_DOT, swz64(drow, 2 * kt + g)), dva[dt]);
-          dka[dt] = mfma32x32x16(sf[kt], lds_read_b128(buf + OFF_QT, swz64(drow, 2 * kt + g)), dka[dt]);
+          dva[dt] = mfma32x32x16(pf1[kt], lds_read_b128(buf + OFF_DOT, swz128(drow, 4 + 2 * kt + g)), dva[dt]);
+          dka[dt] = mfma32x32x16(sf1[kt], lds_read_b128(buf + OFF_QT, swz128(drow, 4 + 2 * kt + g)), dka[dt]);
         }
       }
     }
@@ -247,7 +283,7 @@ __device__ __forceinline__ void issue_ktile(const char* Kh, const char* Vh, cons
     dma_b128(Kh + off, buf + DQ_OFF_K + blk * 1024);
     dma_b128(Vh + off, buf + DQ_OFF_V + blk * 1024);
     const int crow = 16 * blk + (lane >> 2);
-    dma_b128(Kth + crow * col_bytes + kb * 2u + (((lane & 3) ^ ((crow >> 1) & 3)) << 4),
+    dma_b128(Kth + crow * col_bytes + kb * 2u + (((lane & 3) ^ ((crow >> 2) & 3)) << 4),
              buf + DQ_OFF_KT + blk * 1024);
   }
 }
@@ -287,7 +323,7 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(
       df[s] = *reinterpret_cast<const bf16x8*>(dOc + rowoff + 16 * s);
     }
   }
-  const float lse2 = lse_c[(int64_t)u * Sp + myq] * kLog2e;
+  const float lse2 = lse_c[(int64_t)u * Sp + myq];   // already times log2(e)
   const float Dq = Dc[(int64_t)u * Sp + myq];
 
   f32x16 qacc[4];
@@ -314,23 +350,26 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(
       pacc = mfma32x32x16(lds_read_b128(buf + DQ_OFF_V, swz256(r32, 2 * s + g)), df[s], pacc);
     }
     const bool diag = CAUSAL ? (kb + BKQ - 1 > qw) : (kb + BKQ > Sv);
-    bf16x8 sf[2];
+    float p[16];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      float p = fast_exp2(fmaf(sacc[i], kSl2, -lse2));
-      if (diag) {
+    for (int i = 0; i < 16; ++i) p[i] = fast_exp2(fmaf(sacc[i], kSl2, -lse2));
+    if (diag) {   // wave-uniform
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
         const uint32_t key = kb + 8 * (i >> 2) + 4 * g + (i & 3);
         const bool vis = CAUSAL ? (key <= myq) : (key < Sv);
-        if (!vis) p = 0.f;
+        if (!vis) p[i] = 0.f;
       }
-      sf[i >> 3][i & 7] = (bf16)(p * (pacc[i] - Dq));
     }
+    bf16x8 sf[2];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) sf[i >> 3][i & 7] = (bf16)(p[i] * (pacc[i] - Dq));
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) {
       const int drow = 32 * dt + r32;
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt)
-        qacc[dt] = mfma32x32x16(lds_read_b128(buf + DQ_OFF_KT, swz64(drow, 2 * kt + g)), sf[kt],
+        qacc[dt] = mfma32x32x16(lds_read_b128(buf + DQ_OFF_KT, swz64b(drow, 2 * kt + g)), sf[kt],
                                 qacc[dt]);
     }
   }

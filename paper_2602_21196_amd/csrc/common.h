@@ -77,5 +77,8 @@ __device__ __forceinline__ uint32_t swz128(int r, int c) {
   return r * 128 + ((c ^ (r & 7) ^ ((r >> 3) & 1)) << 4);
 }
 __device__ __forceinline__ uint32_t swz64(int r, int c) { return r * 64 + ((c ^ ((r >> 1) & 3)) << 4); }
+// Rows of 64 B for 64-bank LDS (measured on gfx950): c ^ ((r >> 2) & 3) puts
+// the 16 rows read together in 16 distinct 16-byte bank groups.
+__device__ __forceinline__ uint32_t swz64b(int r, int c) { return r * 64 + ((c ^ ((r >> 2) & 3)) << 4); }
 
 }  // namespace upipe

@@ -17,8 +17,8 @@ hipError_t launch_pack_rows(const bf16* src, int64_t S, int H, int h0, int n,
 // src [n, Sp, d] rows < S  ->  dst [S, H, d] heads h0..h0+n-1.
 hipError_t launch_unpack_rows(const bf16* src, int64_t S, int H, int h0, int n,
                               int64_t Sp, bf16* dst, hipStream_t st);
-// D[n, Sp] = rowsum(a * b) over the head width and lse_c[n, Sp] = the lse
-// rows h0.. of the caller's [Hq, S] array (both zero for rows >= S).  Element
+// D[n, Sp] = rowsum(a * b) over the head width and lse_c[n, Sp] = log2(e)
+// times the lse rows h0.. of the caller's [Hq, S] array (zero for rows >= S).  Element
 // (s, hh, e) of a is a[s * a_row + hh * a_head + e], likewise for b.
 hipError_t launch_rowdot_lse(const bf16* a, int64_t a_row, int64_t a_head,
                              const bf16* b, int64_t b_row, int64_t b_head,
@@ -34,6 +34,7 @@ hipError_t launch_attn_fwd(const bf16* Qc, const bf16* Kp, const bf16* Vt,
                            int h0, int G, int causal, hipStream_t st);
 
 // ---- attention backward (attn_bwd.hip) -----------------------------------
+// lse_c below holds log2(e) * lse (the kernels evaluate exp2).
 // Key/value gradients of the chunk's heads, accumulated in fp32 on top of
 // dK32/dV32 [Hkv, Sp, d] (read unless the chunk holds a group's first head),
 // written back there, or -- when the chunk holds the group's last head --
