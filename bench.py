@@ -5,9 +5,14 @@ upipe_attn_fwd followed by upipe_attn_bwd (pack, flash forward, unpack,
 backward pre-pass, dK/dV, dQ, unpack, for every head chunk) on the
 Llama3-8B per-GPU share at 8-way Ulysses (S = 131072, 4 query heads, 1 kv
 head, d = 128), inputs resident in HBM.  Prints one JSON line.
+`--workload qwen32b_share|llama8b_4m|tiny` times the other attention
+shares; `--workload llama8b_layer` times upipe_layer_fwd + upipe_layer_bwd.
 
 Throughput counts only algorithmic work: 4 d flops per visible causal
-(query, key, head) triple for the forward and 2.5x that for the backward.
+(query, key, head) triple for the forward and 2.5x that for the backward;
+for the layer also 2 flops per multiply-add of the QKV and output
+projections, 3x (forward, data gradient, weight gradient; the backward's
+recomputation of K, V and Q is not credited).
 """
 
 import argparse
@@ -100,22 +105,30 @@ def main():
     from paper_2602_21196_amd import upipe
 
     w = W.WORKLOADS[args.workload]
-    if w.is_layer:
-        print("bench.py times the attention workloads", file=sys.stderr)
-        sys.exit(2)
     dev = "cuda:0"
     S, Hq, Hkv, d, U = w.S, w.Hq, w.Hkv, w.d, args.U
-    q, k, v, do = W.attention_inputs(S, Hq, Hkv, d, w.seed)
-    qd, kd, vd, dod = (t.to(dev) for t in (q, k, v, do))
     fwd_flops, bwd_flops = W.attention_flops(S, Hq, d)
     step_flops = fwd_flops + bwd_flops
+    if w.is_layer:
+        dm = w.d_model
+        x, wqkv, wo, dy = (t.to(dev) for t in W.inputs_for(w))
+        proj_fwd = 2 * S * dm * (Hq + 2 * Hkv) * d + 2 * S * Hq * d * dm
+        step_flops += 3 * proj_fwd
+        ws_f = upipe.workspace(upipe.upipe_layer_fwd_workspace_size(S, dm, Hq, Hkv, d, U), dev)
+        ws_b = upipe.workspace(upipe.upipe_layer_bwd_workspace_size(S, dm, Hq, Hkv, d, U), dev)
 
-    ws_f = upipe.workspace(upipe.upipe_attn_fwd_workspace_size(S, Hq, Hkv, d, U), dev)
-    ws_b = upipe.workspace(upipe.upipe_attn_bwd_workspace_size(S, Hq, Hkv, d, U), dev)
+        def step():
+            y, o, lse = upipe.layer_fwd(x, wqkv, wo, Hq, Hkv, d, U=U, ws=ws_f)
+            upipe.layer_bwd(x, wqkv, wo, o, lse, dy, Hq, Hkv, d, U=U, ws=ws_b)
+    else:
+        q, k, v, do = W.attention_inputs(S, Hq, Hkv, d, w.seed)
+        qd, kd, vd, dod = (t.to(dev) for t in (q, k, v, do))
+        ws_f = upipe.workspace(upipe.upipe_attn_fwd_workspace_size(S, Hq, Hkv, d, U), dev)
+        ws_b = upipe.workspace(upipe.upipe_attn_bwd_workspace_size(S, Hq, Hkv, d, U), dev)
 
-    def step():
-        o, lse = upipe.attn_fwd(qd, kd, vd, causal=True, U=U, ws=ws_f)
-        upipe.attn_bwd(qd, kd, vd, o, lse, dod, causal=True, U=U, ws=ws_b)
+        def step():
+            o, lse = upipe.attn_fwd(qd, kd, vd, causal=True, U=U, ws=ws_f)
+            upipe.attn_bwd(qd, kd, vd, o, lse, dod, causal=True, U=U, ws=ws_b)
 
     for _ in range(args.warmup):
         step()
@@ -159,11 +172,12 @@ def main():
            "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
            "data": "synthetic",
            "config": {"workload": w.name, "S": S, "Hq": Hq, "Hkv": Hkv,
-                      "d": d, "U": U, "causal": True, "seed": w.seed},
+                      "d": d, "U": U, "causal": True, "seed": w.seed,
+                      **({"d_model": w.d_model} if w.is_layer else {})},
            "frac_of_peak": round(value / PEAK_BF16_TFLOPS, 4),
            "roofline": roofline, "kernels": kernels}
 
-    if not args.no_sweep:
+    if not args.no_sweep and not w.is_layer:
         del ws_f, ws_b
         torch.cuda.synchronize()
         # outputs of one fwd+bwd: o, dq [S,Hq,d] bf16, dk, dv [S,Hkv,d] bf16,
@@ -194,7 +208,7 @@ def main():
             "inputs, minus the outputs o, lse, dq, dk, dv: the workspaces")
         out["tflops_vs_U"] = sweep_tf
 
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and not w.is_layer:
         out["cpu_baseline"] = cpu_baseline(w, q, k, v, do, args.cpu_seconds)
     print(json.dumps(out), flush=True)
 

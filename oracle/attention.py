@@ -235,3 +235,81 @@ def attn_bwd_chunked(q, k, v, do, U, causal=True):
             dk[:, g, :] += b[:, 0, :]
             dv[:, g, :] += e[:, 0, :]
     return dq, dk, dv
+
+
+def attn_rows_at(q_rows, pos, k, v, do_rows=None, causal=True):
+    """Forward (and dQ, D when ``do_rows`` is given) for query rows supplied
+    directly with their sequence positions ``pos``.
+
+    The same definition as ``attn_fwd`` / ``attn_bwd_rows``; only the listed
+    rows of q (and dO) are ever needed, so callers with very long sequences
+    pass just those rows.  Returns (o, lse) or (o, lse, dq, D) with the row
+    axis first for o and dq, and [Hq, rows] for lse and D.
+    """
+    q_rows = np.asarray(q_rows, np.float64)
+    k = np.asarray(k, np.float64)
+    v = np.asarray(v, np.float64)
+    pos = np.asarray(pos, np.int64)
+    R, Hq, d = q_rows.shape
+    Hkv = k.shape[1]
+    if Hq % Hkv:
+        raise ValueError("Hq must be a multiple of Hkv")
+    o = np.zeros((R, Hq, d))
+    lse = np.zeros((Hq, R))
+    want_grad = do_rows is not None
+    if want_grad:
+        do_rows = np.asarray(do_rows, np.float64)
+        dq = np.zeros((R, Hq, d))
+        Dout = np.zeros((Hq, R))
+    for h in range(Hq):
+        g = kv_head_of(h, Hq, Hkv)
+        for b0 in range(0, R, ROW_BLOCK):
+            sl = slice(b0, min(R, b0 + ROW_BLOCK))
+            s, n = _scores(q_rows[sl, h, :], pos[sl], k[:, g, :], causal, d)
+            m = s.max(axis=1, keepdims=True)
+            e = np.exp(s - m)
+            l = e.sum(axis=1, keepdims=True)
+            o[sl, h, :] = (e / l) @ v[:n, g, :]
+            lse[h, sl] = (m + np.log(l))[:, 0]
+            if want_grad:
+                D = np.sum(do_rows[sl, h, :] * o[sl, h, :], axis=1)
+                p = np.exp(s - lse[h, sl][:, None])
+                dp = do_rows[sl, h, :] @ v[:n, g, :].T
+                ds = p * (dp - D[:, None])
+                dq[sl, h, :] = (ds @ k[:n, g, :]) / np.sqrt(d)
+                Dout[h, sl] = D
+    if want_grad:
+        return o, lse, dq, Dout
+    return o, lse
+
+
+def attn_key_tail_at(q_tail, do_tail, k, v, j0):
+    """dK, dV of causal attention for keys [j0, S) from the query and
+    upstream-gradient rows [j0, S) only (same definition as
+    ``attn_bwd_key_tail``)."""
+    q_tail = np.asarray(q_tail, np.float64)
+    do_tail = np.asarray(do_tail, np.float64)
+    k = np.asarray(k, np.float64)
+    v = np.asarray(v, np.float64)
+    S, Hkv, d = k.shape
+    Hq = q_tail.shape[1]
+    pos = np.arange(j0, S)
+    dk = np.zeros((S - j0, Hkv, d))
+    dv = np.zeros((S - j0, Hkv, d))
+    for h in range(Hq):
+        g = kv_head_of(h, Hq, Hkv)
+        for b0 in range(0, len(pos), ROW_BLOCK):
+            sl = slice(b0, min(len(pos), b0 + ROW_BLOCK))
+            s, n = _scores(q_tail[sl, h, :], pos[sl], k[:, g, :], True, d)
+            m = s.max(axis=1, keepdims=True)
+            e = np.exp(s - m)
+            l = e.sum(axis=1, keepdims=True)
+            o = (e / l) @ v[:n, g, :]
+            lse = m + np.log(l)
+            D = np.sum(do_tail[sl, h, :] * o, axis=1)
+            p = np.exp(s - lse)
+            dp = do_tail[sl, h, :] @ v[:n, g, :].T
+            ds = p * (dp - D[:, None])
+            dk[:n - j0, g, :] += (ds[:, j0:].T @ q_tail[sl, h, :]) / np.sqrt(d)
+            dv[:n - j0, g, :] += p[:, j0:].T @ do_tail[sl, h, :]
+    return dk, dv

@@ -54,3 +54,20 @@ def test_shape_errors():
     q, k, v, _ = _inputs(5, 3, 2, 4, 0)
     with pytest.raises(ValueError):
         A.attn_fwd(q, k, v)
+
+
+def test_row_helpers_with_positions_match_full():
+    q, k, v, do = _inputs(520, 4, 2, 16, 9)
+    o, lse = A.attn_fwd(q, k, v)
+    dq, dk, dv = A.attn_bwd(q, k, v, do)
+    rows = np.array([0, 3, 257, 300, 519])
+    o_r, lse_r, dq_r, D_r = A.attn_rows_at(q[rows], rows, k, v, do[rows])
+    np.testing.assert_allclose(o_r, o[rows], atol=1e-14)
+    np.testing.assert_allclose(lse_r, lse[:, rows], atol=1e-14)
+    np.testing.assert_allclose(dq_r, dq[rows], atol=1e-13)
+    np.testing.assert_allclose(D_r, np.sum(do * o, axis=2).T[:, rows], atol=1e-13)
+    o2, lse2 = A.attn_rows_at(q[rows], rows, k, v)
+    np.testing.assert_array_equal(o2, o_r)
+    dk_t, dv_t = A.attn_key_tail_at(q[400:], do[400:], k, v, 400)
+    np.testing.assert_allclose(dk_t, dk[400:], atol=1e-12)
+    np.testing.assert_allclose(dv_t, dv[400:], atol=1e-12)
