@@ -24,8 +24,10 @@ MUTANTS = {
     "no_causal_mask": ("np.arange(n)[None, :] > rows[:, None]",
                        "np.arange(n)[None, :] > n"),
     "gqa_modulo_map": ("return h // (Hq // Hkv)", "return h % Hkv"),
-    "lse_drops_max": ("(m + np.log(l))[:, 0]", "(np.log(l))[:, 0]"),
-    "unnormalised_o": ("(e / l) @ v[:n, g, :]", "e @ v[:n, g, :]"),
+    "lse_drops_max": ("lse[h, b0:b0 + len(r)] = (m + np.log(l))[:, 0]",
+                      "lse[h, b0:b0 + len(r)] = (np.log(l))[:, 0]"),
+    "unnormalised_o": ("o[b0:b0 + len(r), h, :] = (e / l) @ v[:n, g, :]",
+                       "o[b0:b0 + len(r), h, :] = e @ v[:n, g, :]"),
     "ds_sign": ("ds = p * (dp - D[r][:, None])",
                 "ds = p * (dp + D[r][:, None])"),
     "dk_no_scale": ("dk[:n, g, :] += (ds.T @ q[r, h, :]) * scale",
