@@ -27,6 +27,9 @@ if ROOT not in sys.path:
 
 METRIC = ("attention fwd+bwd TFLOP/s (causal) per MI355X; "
           "peak activation GB vs chunk size U")
+KERNEL_SOURCES = {"attn_fwd": ("attn_fwd.hip", "common.h"),
+                  "attn_bwd_dkdv": ("attn_bwd.hip", "common.h"),
+                  "attn_bwd_dq": ("attn_bwd.hip", "common.h")}
 PEAK_BF16_TFLOPS = 2516.6   # 256 CU x 4096 flop/clk x 2.4 GHz, dense bf16
 PEAK_HBM_GBS = 8000.0
 
@@ -54,6 +57,33 @@ def kernel_flops(S, U, d, causal=True):
         "attn_bwd_dkdv": 8 * d * U * pairs,     # S, dP recompute + dV, dK
         "attn_bwd_dq": 2 * d * U * pairs,       # dQ (S, dP recomputed again)
     }
+
+
+def source_sha(kernel):
+    """Hash of the sources a kernel is built from (traffic records go stale
+    when they change)."""
+    import hashlib
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(ROOT, "paper_2602_21196_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel, workload, U):
+    """HBM bytes per launch from profiles/traffic.json (rocprofv3 FETCH_SIZE
+    and WRITE_SIZE, calibrated on a copy kernel), if they were taken on the
+    current source of that kernel for this workload; else None."""
+    import json as _json
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        with open(path) as f:
+            rec = _json.load(f).get(f"{workload}/U{U}/{kernel}")
+    except (OSError, ValueError):
+        return None
+    if not rec or rec.get("source_sha") != source_sha(kernel):
+        return None
+    return rec["fetch_bytes"] + rec["write_bytes"]
 
 
 def cpu_baseline(w, q, k, v, do, target_s):
@@ -163,7 +193,9 @@ def main():
                 "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
                 "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_BF16_TFLOPS, 4) if achieved else None,
-                "traffic": None}
+                "traffic": (measured_traffic(dom, w.name, U)
+                            if dom in KERNEL_SOURCES else None),
+                "traffic_unit": "bytes per launch"}
     upipe.upipe_profile_reset()
 
     out = {"metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s",

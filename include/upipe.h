@@ -60,7 +60,8 @@ typedef enum {
   UPIPE_ERR_INVALID_ARG = -1, /* bad size, null/misaligned pointer, U or Hkv
                                  not dividing Hq, workspace too small      */
   UPIPE_ERR_UNSUPPORTED = -2, /* valid in principle, not built: d != 128,
-                                 d_model % 128 != 0, Hq > 64, too large     */
+                                 d_model % 128 != 0, Hq > 64, S rounded up
+                                 to a multiple of 128 above 2^24 - 128      */
   UPIPE_ERR_WORKSPACE = -3,   /* ws_bytes below the size query's result     */
   UPIPE_ERR_HIP = -4          /* a HIP runtime call or launch failed        */
 } upipe_status;

@@ -9,7 +9,10 @@
 namespace upipe {
 
 constexpr int kMaxHeads = 64;
-constexpr int64_t kMaxSeq = int64_t(1) << 30;
+// Longest padded sequence: the kernels address one head's [Sp][128] slab and
+// its [128][Sp] transpose with 32-bit byte offsets and buffer resources of
+// Sp * 256 bytes, which must stay below 2^32.
+constexpr int64_t kMaxSeq = (int64_t(1) << 24) - SEQ_PAD;
 
 // Kernel families for event timing; order matches kFamilyNames in api.cpp.
 enum Family {

@@ -17,8 +17,8 @@
 //         left in the workspace (UPipe keeps per-group dK/dV accumulators alive
 //         across stages, Appendix A), so any chunk size U gives bit-identical
 //         sums.
-//   dq:   a workgroup owns 128 query rows of one head and walks 32-key tiles
-//         in ascending order, recomputing P and dS.
+//   dq:   a workgroup owns 256 query rows of one head (8 waves) and walks
+//         64-key stages in ascending order, recomputing P and dS.
 // Tiles reach LDS through direct global->LDS copies issued one tile ahead.
 // Transposed operands come from the MFMA-ordered [d][S] copies (common.h).
 #include "common.h"
@@ -42,49 +42,73 @@ constexpr int OFF_Q = 0, OFF_DO = ROWT, OFF_QT = 2 * ROWT, OFF_DOT = 3 * ROWT,
               OFF_LSE = 4 * ROWT, OFF_D = OFF_LSE + QT * 4;
 constexpr int KV_STAGE = 4 * ROWT + 1024;   // lse/D block padded to 1 KB
 
-struct QTilePtrs {
-  const char *q, *dO, *qt, *dOt, *lse, *D;   // head bases (bytes)
-  uint32_t col_bytes;                          // row stride of the [d][Sp] copies
+// This wave's share of one stage's copies: four 1 KB blocks each of Q and dO
+// (4 rows of 256 B) and of Q^T and dO^T (8 rows of 128 B); wave 0 also copies
+// the 64 lse and D values.  `qoff` is the tile's uniform row offset in the
+// head's buffers, `offr` / `offc` the lane offsets of the row and column blocks.
+struct QStageSrc {
+  buf_rsrc q, dO, qt, dOt, lse, D;
 };
 
-// Wave w copies four 1 KB blocks of each of Q, dO (4 rows of 256 B per block)
-// and Q^T, dO^T (8 rows of 128 B per block); wave 0 also copies lse and D.
-__device__ __forceinline__ void issue_qtile(const QTilePtrs& p, uint32_t qb, char* buf, int w,
-                                            int lane) {
+__device__ __forceinline__ void issue_qstage(const QStageSrc& r, const uint32_t (&offr)[4],
+                                             const uint32_t (&offc)[4], uint32_t qb, char* buf,
+                                             int w, int lane) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int blk = 4 * w + i;
-    const int row = 4 * blk + (lane >> 4);
-    const uint32_t off = (qb + row) * 256u + (((lane & 15) ^ (row & 15)) << 4);
-    dma_b128(p.q + off, buf + OFF_Q + blk * 1024);
-    dma_b128(p.dO + off, buf + OFF_DO + blk * 1024);
-    const int crow = 8 * blk + (lane >> 3);
-    const uint32_t coff = crow * p.col_bytes + qb * 2u +
-                          (((lane & 7) ^ (crow & 7) ^ ((crow >> 3) & 1)) << 4);
-    dma_b128(p.qt + coff, buf + OFF_QT + blk * 1024);
-    dma_b128(p.dOt + coff, buf + OFF_DOT + blk * 1024);
+    dma_buf_b128(r.q, offr[i], qb * 256u, buf + OFF_Q + blk * 1024);
+    dma_buf_b128(r.dO, offr[i], qb * 256u, buf + OFF_DO + blk * 1024);
+    dma_buf_b128(r.qt, offc[i], qb * 2u, buf + OFF_QT + blk * 1024);
+    dma_buf_b128(r.dOt, offc[i], qb * 2u, buf + OFF_DOT + blk * 1024);
   }
   if (w == 0 && lane < 32) {
-    const char* src = lane < 16 ? p.lse + qb * 4u + lane * 16u : p.D + qb * 4u + (lane - 16) * 16u;
-    dma_b128(src, buf + OFF_LSE);
+    // lanes 0..15: lse[qb .. qb+63], lanes 16..31: D[qb .. qb+63]
+    const uint32_t off = (uint32_t)(lane & 15) * 16u;
+    dma_buf_b128(lane < 16 ? r.lse : r.D, off, qb * 4u, buf + OFF_LSE);
   }
 }
 
-// One 32-row query subtile: rows qs..qs+31 at offset `sub` (0 or 32) in the
-// stage.  Returns the bf16 P and dS fragments for the dV / dK products.
+// Operand fragments of one block of 16 MFMAs.
+struct Frags {
+  bf16x8 f[16];
+};
+
+// S^T / dP^T block of one 32-row subtile (rows `sub`..+31 of the stage):
+// fragment 2 s + 0 is Q, 2 s + 1 is dO, both for head-dim 16 s..
+__device__ __forceinline__ void read_sdp(const char* buf, int sub, int r32, int g, Frags& fr) {
+#pragma unroll
+  for (int s = 0; s < 8; ++s) {
+    fr.f[2 * s] = lds_read_b128(buf + OFF_Q, swz256(sub + r32, 2 * s + g));
+    fr.f[2 * s + 1] = lds_read_b128(buf + OFF_DO, swz256(sub + r32, 2 * s + g));
+  }
+}
+
+// dV / dK block of one subtile: fragment 4 dt + 2 kt + 0 is dO^T, + 1 is Q^T,
+// head-dim rows 32 dt.., query chunk kt of the subtile.
+__device__ __forceinline__ void read_dvdk(const char* buf, int sub, int r32, int g, Frags& fr) {
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) {
+      const uint32_t off = swz128(32 * dt + r32, (sub >> 3) + 2 * kt + g);
+      fr.f[4 * dt + 2 * kt] = lds_read_b128(buf + OFF_DOT, off);
+      fr.f[4 * dt + 2 * kt + 1] = lds_read_b128(buf + OFF_QT, off);
+    }
+}
+
+// Scores of one subtile from its fragments, then P and dS (bf16 B operands).
 template <bool CAUSAL>
-__device__ __forceinline__ void subtile_scores(const char* buf, int sub, uint32_t qs,
-                                               uint32_t mykey, bool diag, int r32, int g,
-                                               const bf16x8 (&kf)[8], const bf16x8 (&vf)[8],
-                                               bf16x8 (&pf)[2], bf16x8 (&sf)[2]) {
+__device__ __forceinline__ void subtile_pds(const Frags& fr, const char* buf, int sub, uint32_t qs,
+                                            uint32_t mykey, bool diag, int g,
+                                            const bf16x8 (&kf)[8], const bf16x8 (&vf)[8],
+                                            bf16x8 (&pf)[2], bf16x8 (&sf)[2]) {
   f32x16 sacc, pacc;
 #pragma unroll
   for (int i = 0; i < 16; ++i) { sacc[i] = 0.f; pacc[i] = 0.f; }
-  const int row = sub + r32;
 #pragma unroll
   for (int s = 0; s < 8; ++s) {
-    sacc = mfma32x32x16(lds_read_b128(buf + OFF_Q, swz256(row, 2 * s + g)), kf[s], sacc);
-    pacc = mfma32x32x16(lds_read_b128(buf + OFF_DO, swz256(row, 2 * s + g)), vf[s], pacc);
+    sacc = mfma32x32x16(fr.f[2 * s], kf[s], sacc);
+    pacc = mfma32x32x16(fr.f[2 * s + 1], vf[s], pacc);
   }
   const float* lsel = reinterpret_cast<const float*>(buf + OFF_LSE) + sub;
   const float* Dl = reinterpret_cast<const float*>(buf + OFF_D) + sub;
@@ -112,6 +136,18 @@ __device__ __forceinline__ void subtile_scores(const char* buf, int sub, uint32_
   }
 }
 
+__device__ __forceinline__ void dvdk_products(const Frags& fr, const bf16x8 (&pf)[2],
+                                              const bf16x8 (&sf)[2], f32x16 (&dva)[4],
+                                              f32x16 (&dka)[4]) {
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) {
+      dva[dt] = mfma32x32x16(pf[kt], fr.f[4 * dt + 2 * kt], dva[dt]);
+      dka[dt] = mfma32x32x16(sf[kt], fr.f[4 * dt + 2 * kt + 1], dka[dt]);
+    }
+}
+
 template <bool CAUSAL>
 __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(
     const bf16* __restrict__ Qc, const bf16* __restrict__ Qct, const bf16* __restrict__ dOc,
@@ -121,36 +157,46 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(
     int U, int h0, int G, int Hkv) {
   __shared__ __attribute__((aligned(1024))) char smem[2 * KV_STAGE];
   const int t = threadIdx.x;
-  const int lane = t & 63, w = t >> 6;
+  const int lane = t & 63;
+  const int w = __builtin_amdgcn_readfirstlane(t >> 6);
   const int r32 = lane & 31, g = lane >> 5;
   const int kvh = h0 / G + blockIdx.y;
   const uint32_t kb0 = blockIdx.x * 128u;
   const uint32_t kw = kb0 + 32 * w;      // first key of this wave
   const uint32_t mykey = kw + r32;       // key column owned by this lane
+  const uint32_t Spv = (uint32_t)Sp;
   const int hlo = max(h0, kvh * G), hhi = min(h0 + U, (kvh + 1) * G);
   const bool first = kvh * G >= h0;           // no earlier chunk touched kvh
   const bool last = (kvh + 1) * G <= h0 + U;  // no later chunk will
-  const uint32_t nqt = (uint32_t)(Sp / QT);
+  const uint32_t nqt = Spv / QT;
   const uint32_t qt_lo = CAUSAL ? kb0 / QT : 0;   // lowest query tile needed
   const uint32_t per_head = nqt - qt_lo;
   const int total = (int)(per_head * (hhi - hlo));
 
-  auto ptrs = [&](int hh) {
-    QTilePtrs p;
+  uint32_t offr[4], offc[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int blk = 4 * w + i;
+    const int r = 4 * blk + (lane >> 4);      // Q / dO row of the tile, 16 lanes per row
+    offr[i] = r * 256u + (((lane & 15) ^ (r & 15)) << 4);
+    const int c = 8 * blk + (lane >> 3);      // Q^T / dO^T row (head-dim), 8 lanes per row
+    offc[i] = c * (Spv * 2u) + (((lane & 7) ^ (c & 7) ^ ((c >> 3) & 1)) << 4);
+  }
+  auto srcs = [&](int hh) {
+    QStageSrc r;
     const int64_t hoff = (int64_t)(hh - h0) * Sp * HEAD_DIM;
-    p.q = reinterpret_cast<const char*>(Qc + hoff);
-    p.dO = reinterpret_cast<const char*>(dOc + hoff);
-    p.qt = reinterpret_cast<const char*>(Qct + hoff);
-    p.dOt = reinterpret_cast<const char*>(dOct + hoff);
-    p.lse = reinterpret_cast<const char*>(lse_c + (int64_t)(hh - h0) * Sp);
-    p.D = reinterpret_cast<const char*>(Dc + (int64_t)(hh - h0) * Sp);
-    p.col_bytes = (uint32_t)Sp * 2u;
-    return p;
+    r.q = make_rsrc(Qc + hoff, Spv * 256u);
+    r.dO = make_rsrc(dOc + hoff, Spv * 256u);
+    r.qt = make_rsrc(Qct + hoff, Spv * 256u);
+    r.dOt = make_rsrc(dOct + hoff, Spv * 256u);
+    r.lse = make_rsrc(lse_c + (int64_t)(hh - h0) * Sp, Spv * 4u);
+    r.D = make_rsrc(Dc + (int64_t)(hh - h0) * Sp, Spv * 4u);
+    return r;
   };
 
   // First tile: head hlo, query tile nqt-1.
-  QTilePtrs cur = ptrs(hlo);
-  issue_qtile(cur, (nqt - 1) * QT, smem, w, lane);
+  QStageSrc cur = srcs(hlo);
+  issue_qstage(cur, offr, offc, (nqt - 1) * QT, smem, w, lane);
 
   // K and V B-operand fragments (lane = key column, k = head dim).
   bf16x8 kf[8], vf[8];
@@ -203,38 +249,29 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(
     wait_vmem();
     __syncthreads();   // this tile landed for all waves; the other buffer is free
     if (it + 1 < total) {
-      if (nh != hh) cur = ptrs(nh);
-      issue_qtile(cur, nq * QT, smem + ((it + 1) & 1) * KV_STAGE, w, lane);
+      if (nh != hh) cur = srcs(nh);
+      issue_qstage(cur, offr, offc, nq * QT, smem + ((it + 1) & 1) * KV_STAGE, w, lane);
     }
 
-    // Subtile 1 (rows qb+32..63) is needed whenever subtile 0 is.
-    const bool need0 = !CAUSAL || qb + 31 >= kw;
-    const bool need1 = !CAUSAL || qb + 63 >= kw;
-    if (need1) {
-      bf16x8 pf1[2], sf1[2];
-      subtile_scores<CAUSAL>(buf, 32, qb + 32, mykey, qb + 32 < kw + 31, r32, g, kf, vf, pf1, sf1);
-      if (need0) {
-        bf16x8 pf0[2], sf0[2];
-        subtile_scores<CAUSAL>(buf, 0, qb, mykey, qb < kw + 31, r32, g, kf, vf, pf0, sf0);
-#pragma unroll
-        for (int dt = 0; dt < 4; ++dt) {
-          const int drow = 32 * dt + r32;
-#pragma unroll
-          for (int kt = 0; kt < 2; ++kt) {
-            dva[dt] = mfma32x32x16(pf0[kt], lds_read_b128(buf + OFF_DOT, swz128(drow, 2 * kt + g)), dva[dt]);
-            dka[dt] = mfma32x32x16(sf0[kt], lds_read_b128(buf + OFF_QT, swz128(drow, 2 * kt + g)), dka[dt]);
-          }
-        }
-      }
-#pragma unroll
-      for (int dt = 0; dt < 4; ++dt) {
-        const int drow = 32 * dt + r32;
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt) {
-          dva[dt] = mfma32x32x16(pf1[kt], lds_read_b128(buf + OFF_DOT, swz128(drow, 4 + 2 * kt + g)), dva[dt]);
-          dka[dt] = mfma32x32x16(sf1[kt], lds_read_b128(buf + OFF_QT, swz128(drow, 4 + 2 * kt + g)), dka[dt]);
-        }
-      }
+    // Causal: a tile is needed when its last row reaches this wave's first
+    // key; on the one tile where only its second subtile does, the first is
+    // computed under the diagonal mask, which zeroes all of its P and dS.
+    // Each block of 16 MFMAs finds its LDS fragments already read: the reads
+    // of the next block are issued before the products of the current one.
+    if (!CAUSAL || qb + 63 >= kw) {
+      Frags fa, fb;
+      bf16x8 pf1[2], sf1[2], pf0[2], sf0[2];
+      read_sdp(buf, 32, r32, g, fa);
+      read_sdp(buf, 0, r32, g, fb);
+      __builtin_amdgcn_sched_barrier(0);
+      subtile_pds<CAUSAL>(fa, buf, 32, qb + 32, mykey, qb + 32 < kw + 31, g, kf, vf, pf1, sf1);
+      read_dvdk(buf, 0, r32, g, fa);
+      __builtin_amdgcn_sched_barrier(0);
+      subtile_pds<CAUSAL>(fb, buf, 0, qb, mykey, qb < kw + 31, g, kf, vf, pf0, sf0);
+      read_dvdk(buf, 32, r32, g, fb);
+      __builtin_amdgcn_sched_barrier(0);
+      dvdk_products(fa, pf0, sf0, dva, dka);
+      dvdk_products(fb, pf1, sf1, dva, dka);
     }
     qt = nq;
     hh = nh;
@@ -265,66 +302,84 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(
 }
 
 // ---------------------------------------------------------------------- dQ
-// LDS stage for one 32-key tile: K [32][128], V [32][128] (256-B rows) and
-// K^T [128][32] in MFMA order (64-B rows).
-constexpr int BKQ = 32;
-constexpr int KT8 = BKQ * HEAD_DIM * 2;   // 8 KB
-constexpr int DQ_OFF_K = 0, DQ_OFF_V = KT8, DQ_OFF_KT = 2 * KT8;
-constexpr int DQ_STAGE = 3 * KT8;
+// Workgroup = 8 waves x 32 query rows (256 rows, two waves per SIMD).  LDS
+// stage for one 64-key tile: K [64][128], V [64][128] (256-B rows) and K^T
+// [128][64] in MFMA order (128-B rows); a stage is consumed as two 32-key
+// subtiles, keys ascending.
+constexpr int DQ_BQ = 256;
+constexpr int DQ_BK = 64;
+constexpr int DQ_T = DQ_BK * HEAD_DIM * 2;   // 16 KB
+constexpr int DQ_OFF_K = 0, DQ_OFF_V = DQ_T, DQ_OFF_KT = 2 * DQ_T;
+constexpr int DQ_STAGE = 3 * DQ_T;
 
-__device__ __forceinline__ void issue_ktile(const char* Kh, const char* Vh, const char* Kth,
-                                            uint32_t col_bytes, uint32_t kb, char* buf, int w,
-                                            int lane) {
+// This wave's share of one stage's copies: 2 blocks of 1 KB each of K rows,
+// V rows (4 rows of 256 B) and K^T rows (8 rows of 128 B).
+__device__ __forceinline__ void issue_kstage(buf_rsrc rk, buf_rsrc rv, buf_rsrc rkt,
+                                             const uint32_t (&offr)[2], const uint32_t (&offt)[2],
+                                             uint32_t kb, char* buf, int w) {
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const int blk = 2 * w + i;
-    const int row = 4 * blk + (lane >> 4);
-    const uint32_t off = (kb + row) * 256u + (((lane & 15) ^ (row & 15)) << 4);
-    dma_b128(Kh + off, buf + DQ_OFF_K + blk * 1024);
-    dma_b128(Vh + off, buf + DQ_OFF_V + blk * 1024);
-    const int crow = 16 * blk + (lane >> 2);
-    dma_b128(Kth + crow * col_bytes + kb * 2u + (((lane & 3) ^ ((crow >> 2) & 3)) << 4),
-             buf + DQ_OFF_KT + blk * 1024);
+    dma_buf_b128(rk, offr[i], kb * 256u, buf + DQ_OFF_K + blk * 1024);
+    dma_buf_b128(rv, offr[i], kb * 256u, buf + DQ_OFF_V + blk * 1024);
+    dma_buf_b128(rkt, offt[i], kb * 2u, buf + DQ_OFF_KT + blk * 1024);
   }
 }
 
 template <bool CAUSAL>
-__global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(
+__global__ __launch_bounds__(512, 1) void attn_bwd_dq_kernel(
     const bf16* __restrict__ Qc, const bf16* __restrict__ dOc, const float* __restrict__ lse_c,
     const float* __restrict__ Dc, const bf16* __restrict__ Kp, const bf16* __restrict__ Kt,
     const bf16* __restrict__ Vp, bf16* __restrict__ dQc, int64_t S, int64_t Sp, int U, int h0,
     int G, int nqb) {
   __shared__ __attribute__((aligned(1024))) char smem[2 * DQ_STAGE];
   const int t = threadIdx.x;
-  const int lane = t & 63, w = t >> 6;
+  const int lane = t & 63;
+  const int w = __builtin_amdgcn_readfirstlane(t >> 6);
   const int r32 = lane & 31, g = lane >> 5;
   const int L = blockIdx.x;
   const int qb = nqb - 1 - L / U;
   const int u = L % U;
   const int kvh = (h0 + u) / G;
-  const uint32_t q0 = (uint32_t)qb * 128;
+  const uint32_t Spv = (uint32_t)Sp;
+  const uint32_t q0 = (uint32_t)qb * DQ_BQ;
   const uint32_t qw = q0 + 32 * w;
   const uint32_t myq = qw + r32;
   const uint32_t Sv = (uint32_t)S;
+  const bool rows_ok = qw < Spv;            // the last block may hold 128 rows only
 
-  const char* Kh = reinterpret_cast<const char*>(Kp + (int64_t)kvh * Sp * HEAD_DIM);
-  const char* Vh = reinterpret_cast<const char*>(Vp + (int64_t)kvh * Sp * HEAD_DIM);
-  const char* Kth = reinterpret_cast<const char*>(Kt + (int64_t)kvh * HEAD_DIM * Sp);
-  const uint32_t col_bytes = (uint32_t)Sp * 2u;
-  const int ntiles = CAUSAL ? (int)((q0 + 128) / BKQ) : (int)(Sp / BKQ);
-  issue_ktile(Kh, Vh, Kth, col_bytes, 0, smem, w, lane);
+  // One head's K and V rows [Sp][128] and K^T rows [128][Sp], 32-bit addressed.
+  const buf_rsrc rk = make_rsrc(Kp + (int64_t)kvh * Sp * HEAD_DIM, Spv * 256u);
+  const buf_rsrc rv = make_rsrc(Vp + (int64_t)kvh * Sp * HEAD_DIM, Spv * 256u);
+  const buf_rsrc rkt = make_rsrc(Kt + (int64_t)kvh * HEAD_DIM * Sp, Spv * 256u);
+  uint32_t offr[2], offt[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int blk = 2 * w + i;
+    const int r = 4 * blk + (lane >> 4);      // K/V row of the stage, 16 lanes per row
+    offr[i] = r * 256u + (((lane & 15) ^ (r & 15)) << 4);
+    const int c = 8 * blk + (lane >> 3);      // K^T row (head-dim), 8 lanes per row
+    offt[i] = c * (Spv * 2u) + (((lane & 7) ^ (c & 7) ^ ((c >> 3) & 1)) << 4);
+  }
+  const int nst = CAUSAL ? (int)(min(q0 + DQ_BQ, Spv) / DQ_BK) : (int)(Spv / DQ_BK);
+  issue_kstage(rk, rv, rkt, offr, offt, 0, smem, w);
 
   bf16x8 qf[8], df[8];
-  {
+  float lse2 = 0.f, Dq = 0.f;
+#pragma unroll
+  for (int s = 0; s < 8; ++s)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) { qf[s][e] = (bf16)0.f; df[s][e] = (bf16)0.f; }
+  if (rows_ok) {
     const int64_t rowoff = ((int64_t)u * Sp + myq) * HEAD_DIM + 8 * g;
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
       qf[s] = *reinterpret_cast<const bf16x8*>(Qc + rowoff + 16 * s);
       df[s] = *reinterpret_cast<const bf16x8*>(dOc + rowoff + 16 * s);
     }
+    lse2 = lse_c[(int64_t)u * Sp + myq];   // already times log2(e)
+    Dq = Dc[(int64_t)u * Sp + myq];
   }
-  const float lse2 = lse_c[(int64_t)u * Sp + myq];   // already times log2(e)
-  const float Dq = Dc[(int64_t)u * Sp + myq];
 
   f32x16 qacc[4];
 #pragma unroll
@@ -332,48 +387,54 @@ __global__ __launch_bounds__(256, 2) void attn_bwd_dq_kernel(
 #pragma unroll
     for (int i = 0; i < 16; ++i) qacc[dt][i] = 0.f;
 
-  for (int j = 0; j < ntiles; ++j) {
-    const uint32_t kb = (uint32_t)j * BKQ;
+  for (int j = 0; j < nst; ++j) {
+    const uint32_t ks = (uint32_t)j * DQ_BK;
     char* buf = smem + (j & 1) * DQ_STAGE;
     wait_vmem();
-    __syncthreads();
-    if (j + 1 < ntiles)
-      issue_ktile(Kh, Vh, Kth, col_bytes, kb + BKQ, smem + ((j + 1) & 1) * DQ_STAGE, w, lane);
-    if (CAUSAL && kb > qw + 31) continue;
-
-    f32x16 sacc, pacc;
+    __syncthreads();   // stage j landed for all waves; stage j-1's buffer is free
+    if (j + 1 < nst) issue_kstage(rk, rv, rkt, offr, offt, ks + DQ_BK, smem + ((j + 1) & 1) * DQ_STAGE, w);
+    if (!rows_ok) continue;
+    if (CAUSAL && ks > qw + 31) continue;    // whole stage masked for this wave
+    f32x16 sacc[2], pacc[2];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) { sacc[i] = 0.f; pacc[i] = 0.f; }
+    for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
-    for (int s = 0; s < 8; ++s) {
-      sacc = mfma32x32x16(lds_read_b128(buf + DQ_OFF_K, swz256(r32, 2 * s + g)), qf[s], sacc);
-      pacc = mfma32x32x16(lds_read_b128(buf + DQ_OFF_V, swz256(r32, 2 * s + g)), df[s], pacc);
-    }
-    const bool diag = CAUSAL ? (kb + BKQ - 1 > qw) : (kb + BKQ > Sv);
-    float p[16];
+      for (int i = 0; i < 16; ++i) { sacc[hh][i] = 0.f; pacc[hh][i] = 0.f; }
 #pragma unroll
-    for (int i = 0; i < 16; ++i) p[i] = fast_exp2(fmaf(sacc[i], kSl2, -lse2));
-    if (diag) {   // wave-uniform
+    for (int s = 0; s < 8; ++s)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const uint32_t key = kb + 8 * (i >> 2) + 4 * g + (i & 3);
-        const bool vis = CAUSAL ? (key <= myq) : (key < Sv);
-        if (!vis) p[i] = 0.f;
+      for (int hh = 0; hh < 2; ++hh) {
+        const int row = 32 * hh + r32;
+        sacc[hh] = mfma32x32x16(lds_read_b128(buf + DQ_OFF_K, swz256(row, 2 * s + g)), qf[s], sacc[hh]);
+        pacc[hh] = mfma32x32x16(lds_read_b128(buf + DQ_OFF_V, swz256(row, 2 * s + g)), df[s], pacc[hh]);
       }
+    const bool diag = CAUSAL ? (ks + DQ_BK - 1 > qw) : (ks + DQ_BK > Sv);
+    bf16x8 sf[2][2];
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      float p[16];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) p[i] = fast_exp2(fmaf(sacc[hh][i], kSl2, -lse2));
+      if (diag) {   // wave-uniform
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const uint32_t key = ks + 32 * hh + 8 * (i >> 2) + 4 * g + (i & 3);
+          const bool vis = CAUSAL ? (key <= myq) : (key < Sv);
+          if (!vis) p[i] = 0.f;
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < 16; ++i) sf[hh][i >> 3][i & 7] = (bf16)(p[i] * (pacc[hh][i] - Dq));
     }
-    bf16x8 sf[2];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) sf[i >> 3][i & 7] = (bf16)(p[i] * (pacc[i] - Dq));
+    for (int c = 0; c < 4; ++c)
 #pragma unroll
-    for (int dt = 0; dt < 4; ++dt) {
-      const int drow = 32 * dt + r32;
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-        qacc[dt] = mfma32x32x16(lds_read_b128(buf + DQ_OFF_KT, swz64b(drow, 2 * kt + g)), sf[kt],
-                                qacc[dt]);
-    }
+      for (int dt = 0; dt < 4; ++dt)
+        qacc[dt] = mfma32x32x16(lds_read_b128(buf + DQ_OFF_KT, swz128(32 * dt + r32, 2 * c + g)),
+                                sf[c >> 1][c & 1], qacc[dt]);
   }
 
+  if (!rows_ok) return;
   bf16* op = dQc + ((int64_t)u * Sp + myq) * HEAD_DIM + 4 * g;
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt)
@@ -407,13 +468,13 @@ hipError_t launch_attn_bwd_dkdv(const bf16* Qc, const bf16* Qct, const bf16* dOc
 hipError_t launch_attn_bwd_dq(const bf16* Qc, const bf16* dOc, const float* lse_c, const float* D,
                               const bf16* Kp, const bf16* Kt, const bf16* Vp, bf16* dQc, int64_t S,
                               int64_t Sp, int U, int h0, int G, int causal, hipStream_t st) {
-  const int nqb = (int)(Sp / 128);
+  const int nqb = (int)((Sp + DQ_BQ - 1) / DQ_BQ);
   dim3 grid((unsigned)(nqb * U));
   if (causal)
-    hipLaunchKernelGGL(attn_bwd_dq_kernel<true>, grid, dim3(256), 0, st, Qc, dOc, lse_c, D, Kp, Kt,
+    hipLaunchKernelGGL(attn_bwd_dq_kernel<true>, grid, dim3(512), 0, st, Qc, dOc, lse_c, D, Kp, Kt,
                        Vp, dQc, S, Sp, U, h0, G, nqb);
   else
-    hipLaunchKernelGGL(attn_bwd_dq_kernel<false>, grid, dim3(256), 0, st, Qc, dOc, lse_c, D, Kp,
+    hipLaunchKernelGGL(attn_bwd_dq_kernel<false>, grid, dim3(512), 0, st, Qc, dOc, lse_c, D, Kp,
                        Kt, Vp, dQc, S, Sp, U, h0, G, nqb);
   return hipGetLastError();
 }

@@ -25,6 +25,7 @@ namespace upipe {
 typedef __bf16 bf16;
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -62,6 +63,21 @@ __device__ __forceinline__ void lds_write_b128(char* base, uint32_t off, u32x4 v
 typedef __attribute__((address_space(3))) void lds_void;
 __device__ __forceinline__ void dma_b128(const void* g, char* lds_wave_base) {
   __builtin_amdgcn_global_load_lds(g, (lds_void*)lds_wave_base, 16, 0, 0);
+}
+
+// Raw buffer resource over `bytes` bytes at `base` (stride 0, gfx9 data
+// format word); loads at offsets past `bytes` return zeros instead of faulting.
+typedef __amdgpu_buffer_rsrc_t buf_rsrc;
+__device__ __forceinline__ buf_rsrc make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+// Buffer -> LDS copy of 16 bytes per lane (buffer_load_dwordx4 ... lds): the
+// bytes at voff + soff (lane offset + uniform offset) of lane L land at
+// lds_wave_base + 16 * L.  No vector ALU work for the address; tracked by vmcnt.
+__device__ __forceinline__ void dma_buf_b128(buf_rsrc r, uint32_t voff, uint32_t soff,
+                                             char* lds_wave_base) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)lds_wave_base, 16, voff, soff, 0, 0);
 }
 
 // Wait until every outstanding global load of this wave has completed.

@@ -85,6 +85,11 @@ def test_workspace_sizes_follow_the_plan():
     assert upipe.upipe_attn_fwd_workspace_size(1, 1, 1, d, 1) == 4 * 128 * d * 2
     assert upipe.upipe_attn_fwd_workspace_size(0, 1, 1, d, 1) == 0
     assert upipe.upipe_attn_fwd_workspace_size(5, 4, 1, 64, 1) == 0
+    # longest supported share: 2^24 - 128 rows (32-bit per-head byte offsets)
+    smax = (1 << 24) - 128
+    assert upipe.upipe_attn_fwd_workspace_size(smax, 1, 1, d, 1) > 0
+    assert upipe.upipe_attn_fwd_workspace_size(smax + 1, 1, 1, d, 1) == 0
+    assert upipe.upipe_attn_bwd_workspace_size(smax + 1, 1, 1, d, 1) == 0
     # memory grows linearly in U
     sizes = [upipe.upipe_attn_fwd_workspace_size(S, 8, 1, d, U)
              for U in (1, 2, 4, 8)]
