@@ -110,7 +110,7 @@ AttnFwdPlan plan_attn_fwd(int64_t S, int Hq, int Hkv, int U) {
   const size_t head = (size_t)p.Sp * HEAD_DIM * 2;
   Carver c;
   p.Kp = c.take(Hkv * head);
-  p.Vt = c.take(Hkv * head);
+  p.Vp = c.take(Hkv * head);
   p.Qc = c.take(U * head);
   p.Oc = c.take(U * head);
   p.total = c.used;
@@ -124,7 +124,6 @@ AttnBwdPlan plan_attn_bwd(int64_t S, int Hq, int Hkv, int U) {
   const size_t row32 = (size_t)p.Sp * 4;
   Carver c;
   p.Kp = c.take(Hkv * head);
-  p.Kt = c.take(Hkv * head);
   p.Vp = c.take(Hkv * head);
   p.carry = group_split(Hq, Hkv, U);
   if (p.carry) {
@@ -132,9 +131,7 @@ AttnBwdPlan plan_attn_bwd(int64_t S, int Hq, int Hkv, int U) {
     p.dV32 = c.take(Hkv * head * 2);
   }
   p.Qc = c.take(U * head);
-  p.Qct = c.take(U * head);
   p.dOc = c.take(U * head);
-  p.dOct = c.take(U * head);
   p.dQc = c.take(U * head);
   p.D = c.take(U * row32);
   p.lse_c = c.take(U * row32);
@@ -148,18 +145,18 @@ int run_attn_fwd(const bf16* q, const bf16* k, const bf16* v, bf16* o,
                  char* ws, hipStream_t st) {
   const AttnFwdPlan p = plan_attn_fwd(S, Hq, Hkv, U);
   bf16* Kp = (bf16*)(ws + p.Kp);
-  bf16* Vt = (bf16*)(ws + p.Vt);
+  bf16* Vp = (bf16*)(ws + p.Vp);
   bf16* Qc = (bf16*)(ws + p.Qc);
   bf16* Oc = (bf16*)(ws + p.Oc);
   const int G = Hq / Hkv;
   // Key/value heads: packed once, resident for every chunk (on one device
   // the GQA schedule needs each key/value head from its group's first stage
   // on, Section 4.1).
-  UPIPE_LAUNCH(kPackRows, st, launch_pack_rows(k, S, Hkv, 0, Hkv, p.Sp, Kp, nullptr, st));
-  UPIPE_LAUNCH(kPackRows, st, launch_pack_rows(v, S, Hkv, 0, Hkv, p.Sp, nullptr, Vt, st));
+  UPIPE_LAUNCH(kPackRows, st, launch_pack_rows(k, S, Hkv, 0, Hkv, p.Sp, Kp, st));
+  UPIPE_LAUNCH(kPackRows, st, launch_pack_rows(v, S, Hkv, 0, Hkv, p.Sp, Vp, st));
   for (int h0 = 0; h0 < Hq; h0 += U) {
-    UPIPE_LAUNCH(kPackRows, st, launch_pack_rows(q, S, Hq, h0, U, p.Sp, Qc, nullptr, st));
-    UPIPE_LAUNCH(kAttnFwd, st, launch_attn_fwd(Qc, Kp, Vt, Oc, lse, S, p.Sp, U, h0, G, causal, st));
+    UPIPE_LAUNCH(kPackRows, st, launch_pack_rows(q, S, Hq, h0, U, p.Sp, Qc, st));
+    UPIPE_LAUNCH(kAttnFwd, st, launch_attn_fwd(Qc, Kp, Vp, Oc, lse, S, p.Sp, U, h0, G, causal, st));
     UPIPE_LAUNCH(kUnpackRows, st, launch_unpack_rows(Oc, S, Hq, h0, U, p.Sp, o, st));
   }
   return UPIPE_OK;
@@ -171,33 +168,30 @@ int run_attn_bwd(const bf16* q, const bf16* k, const bf16* v, const bf16* o,
                  char* ws, hipStream_t st) {
   const AttnBwdPlan p = plan_attn_bwd(S, Hq, Hkv, U);
   bf16* Kp = (bf16*)(ws + p.Kp);
-  bf16* Kt = (bf16*)(ws + p.Kt);
   bf16* Vp = (bf16*)(ws + p.Vp);
   float* dK32 = p.carry ? (float*)(ws + p.dK32) : nullptr;
   float* dV32 = p.carry ? (float*)(ws + p.dV32) : nullptr;
   bf16* Qc = (bf16*)(ws + p.Qc);
-  bf16* Qct = (bf16*)(ws + p.Qct);
   bf16* dOc = (bf16*)(ws + p.dOc);
-  bf16* dOct = (bf16*)(ws + p.dOct);
   bf16* dQc = (bf16*)(ws + p.dQc);
   float* D = (float*)(ws + p.D);
   float* lse_c = (float*)(ws + p.lse_c);
   const int G = Hq / Hkv;
-  UPIPE_LAUNCH(kPackRows, st, launch_pack_rows(k, S, Hkv, 0, Hkv, p.Sp, Kp, Kt, st));
-  UPIPE_LAUNCH(kPackRows, st, launch_pack_rows(v, S, Hkv, 0, Hkv, p.Sp, Vp, nullptr, st));
+  UPIPE_LAUNCH(kPackRows, st, launch_pack_rows(k, S, Hkv, 0, Hkv, p.Sp, Kp, st));
+  UPIPE_LAUNCH(kPackRows, st, launch_pack_rows(v, S, Hkv, 0, Hkv, p.Sp, Vp, st));
   for (int h0 = 0; h0 < Hq; h0 += U) {
-    UPIPE_LAUNCH(kPackRows, st, launch_pack_rows(q, S, Hq, h0, U, p.Sp, Qc, Qct, st));
-    UPIPE_LAUNCH(kPackRows, st, launch_pack_rows(dout, S, Hq, h0, U, p.Sp, dOc, dOct, st));
+    UPIPE_LAUNCH(kPackRows, st, launch_pack_rows(q, S, Hq, h0, U, p.Sp, Qc, st));
+    UPIPE_LAUNCH(kPackRows, st, launch_pack_rows(dout, S, Hq, h0, U, p.Sp, dOc, st));
     UPIPE_LAUNCH(kRowdotLse, st,
                  launch_rowdot_lse(dout + h0 * HEAD_DIM, (int64_t)Hq * HEAD_DIM, HEAD_DIM,
                                    o + h0 * HEAD_DIM, (int64_t)Hq * HEAD_DIM, HEAD_DIM, lse, S,
                                    h0, U, p.Sp, D, lse_c, st));
     UPIPE_LAUNCH(kAttnBwdDkdv, st,
-                 launch_attn_bwd_dkdv(Qc, Qct, dOc, dOct, lse_c, D, Kp, Vp, dK32, dV32, dk, dv,
-                                      S, p.Sp, U, h0, G, Hkv, causal, st));
+                 launch_attn_bwd_dkdv(Qc, dOc, lse_c, D, Kp, Vp, dK32, dV32, dk, dv, S, p.Sp, U,
+                                      h0, G, Hkv, causal, st));
     UPIPE_LAUNCH(kAttnBwdDq, st,
-                 launch_attn_bwd_dq(Qc, dOc, lse_c, D, Kp, Kt, Vp, dQc, S, p.Sp, U, h0, G,
-                                    causal, st));
+                 launch_attn_bwd_dq(Qc, dOc, lse_c, D, Kp, Vp, dQc, S, p.Sp, U, h0, G, causal,
+                                    st));
     UPIPE_LAUNCH(kUnpackRows, st, launch_unpack_rows(dQc, S, Hq, h0, U, p.Sp, dq, st));
   }
   return UPIPE_OK;

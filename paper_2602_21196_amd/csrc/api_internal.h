@@ -59,14 +59,14 @@ struct Carver {
 
 struct AttnFwdPlan {
   int64_t Sp = 0;
-  size_t Kp = 0, Vt = 0, Qc = 0, Oc = 0, total = 0;
+  size_t Kp = 0, Vp = 0, Qc = 0, Oc = 0, total = 0;
 };
 
 struct AttnBwdPlan {
   int64_t Sp = 0;
   bool carry = false;  // a key/value group spans several chunks
-  size_t Kp = 0, Kt = 0, Vp = 0, dK32 = 0, dV32 = 0;
-  size_t Qc = 0, Qct = 0, dOc = 0, dOct = 0, dQc = 0, D = 0, lse_c = 0;
+  size_t Kp = 0, Vp = 0, dK32 = 0, dV32 = 0;
+  size_t Qc = 0, dOc = 0, dQc = 0, D = 0, lse_c = 0;
   size_t total = 0;
 };
 

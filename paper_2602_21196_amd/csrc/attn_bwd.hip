@@ -9,18 +9,19 @@
 // Two kernels, no atomics, one fixed summation order:
 //   dkdv: a workgroup owns 128 keys of one key/value head (4 waves x 32 keys,
 //         K and V fragments in registers) and walks the chunk's query heads in
-//         ascending order and, within a head, the 64-row query tiles from the
-//         last one down to its diagonal (the two 32-row halves of a tile in
-//         ascending order), so that all resident workgroups read
-//         the same query tiles at about the same time (shared L2 lines).  Its
+//         ascending order and, within a head, the 128-row query tiles from the
+//         last one down to its diagonal (each tile as 64-row halves, upper
+//         first, and each half as two 32-row subtiles in ascending order), so
+//         that all resident workgroups read the same query tiles at about the
+//         same time (shared L2 lines).  Its
 //         fp32 dK/dV accumulators start from the values the previous chunk
 //         left in the workspace (UPipe keeps per-group dK/dV accumulators alive
 //         across stages, Appendix A), so any chunk size U gives bit-identical
 //         sums.
 //   dq:   a workgroup owns 256 query rows of one head (8 waves) and walks
 //         64-key stages in ascending order, recomputing P and dS.
-// Tiles reach LDS through direct global->LDS copies issued one tile ahead.
-// Transposed operands come from the MFMA-ordered [d][S] copies (common.h).
+// Tiles reach LDS through buffer->LDS copies issued one tile ahead.
+// Transposed operands are read out of row-major tiles (common.h, tr_operand).
 #include "common.h"
 #include "kernels.h"
 
@@ -32,39 +33,35 @@ constexpr float kSl2 = 1.4426950408889634f * 0.08838834764831845f;  // log2(e)/s
 constexpr float kScale = 0.08838834764831845f;                      // 1/sqrt(128)
 
 // ------------------------------------------------------------------ dK / dV
-// LDS stage for one 64-row query tile (two 32-row subtiles): Q [64][128] and
-// dO [64][128] (256-B rows), Q^T and dO^T [128][64] in MFMA order (128-B
-// rows), lse and D [64].  Two subtiles per stage let one subtile's softmax
-// gradient (VALU) overlap the other's products (MFMA) within a wave.
-constexpr int QT = 64;
-constexpr int ROWT = QT * HEAD_DIM * 2;   // 16 KB
-constexpr int OFF_Q = 0, OFF_DO = ROWT, OFF_QT = 2 * ROWT, OFF_DOT = 3 * ROWT,
-              OFF_LSE = 4 * ROWT, OFF_D = OFF_LSE + QT * 4;
-constexpr int KV_STAGE = 4 * ROWT + 1024;   // lse/D block padded to 1 KB
+// LDS stage for one tile of QT query rows of one head: Q and dO rows
+// [QT][128] (256-B rows, transposing-read swizzle), then lse and D [QT].  The
+// B operands of dV += P^T dO and dK += dS^T Q are read out of the rows with
+// transposing LDS reads, so no [d][S] copies of Q and dO are needed.  A tile
+// is consumed as pairs of 32-row subtiles, the upper 64 rows first.
+constexpr int QT = 128;
+constexpr int ROWT = QT * HEAD_DIM * 2;
+constexpr int OFF_Q = 0, OFF_DO = ROWT, OFF_LSE = 2 * ROWT, OFF_D = OFF_LSE + QT * 4;
+constexpr int KV_STAGE = 2 * ROWT + QT * 8;
+constexpr int KV_BLK = ROWT / 1024 / 4;     // 1 KB blocks per wave per array
 
-// This wave's share of one stage's copies: four 1 KB blocks each of Q and dO
-// (4 rows of 256 B) and of Q^T and dO^T (8 rows of 128 B); wave 0 also copies
-// the 64 lse and D values.  `qoff` is the tile's uniform row offset in the
-// head's buffers, `offr` / `offc` the lane offsets of the row and column blocks.
 struct QStageSrc {
-  buf_rsrc q, dO, qt, dOt, lse, D;
+  buf_rsrc q, dO, lse, D;
 };
 
-__device__ __forceinline__ void issue_qstage(const QStageSrc& r, const uint32_t (&offr)[4],
-                                             const uint32_t (&offc)[4], uint32_t qb, char* buf,
-                                             int w, int lane) {
+// This wave's share of one tile's copies: KV_BLK blocks of 1 KB each of Q and
+// dO rows; lanes of wave 0 copy the QT lse values, lanes of wave 1 the QT D
+// values (16 bytes per lane).
+__device__ __forceinline__ void issue_qstage(const QStageSrc& r, const uint32_t (&offr)[KV_BLK],
+                                             uint32_t qb, char* buf, int w, int lane) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int blk = 4 * w + i;
+  for (int i = 0; i < KV_BLK; ++i) {
+    const int blk = KV_BLK * w + i;
     dma_buf_b128(r.q, offr[i], qb * 256u, buf + OFF_Q + blk * 1024);
     dma_buf_b128(r.dO, offr[i], qb * 256u, buf + OFF_DO + blk * 1024);
-    dma_buf_b128(r.qt, offc[i], qb * 2u, buf + OFF_QT + blk * 1024);
-    dma_buf_b128(r.dOt, offc[i], qb * 2u, buf + OFF_DOT + blk * 1024);
   }
-  if (w == 0 && lane < 32) {
-    // lanes 0..15: lse[qb .. qb+63], lanes 16..31: D[qb .. qb+63]
-    const uint32_t off = (uint32_t)(lane & 15) * 16u;
-    dma_buf_b128(lane < 16 ? r.lse : r.D, off, qb * 4u, buf + OFF_LSE);
+  if (lane < QT / 4) {
+    if (w == 0) dma_buf_b128(r.lse, lane * 16u, qb * 4u, buf + OFF_LSE);
+    else if (w == 1) dma_buf_b128(r.D, lane * 16u, qb * 4u, buf + OFF_D);
   }
 }
 
@@ -73,30 +70,29 @@ struct Frags {
   bf16x8 f[16];
 };
 
-// S^T / dP^T block of one 32-row subtile (rows `sub`..+31 of the stage):
+// S^T / dP^T block of one 32-row subtile (rows `sub`..+31 of the tile):
 // fragment 2 s + 0 is Q, 2 s + 1 is dO, both for head-dim 16 s..
 __device__ __forceinline__ void read_sdp(const char* buf, int sub, int r32, int g, Frags& fr) {
 #pragma unroll
   for (int s = 0; s < 8; ++s) {
-    fr.f[2 * s] = lds_read_b128(buf + OFF_Q, swz256(sub + r32, 2 * s + g));
-    fr.f[2 * s + 1] = lds_read_b128(buf + OFF_DO, swz256(sub + r32, 2 * s + g));
+    fr.f[2 * s] = lds_read_b128(buf + OFF_Q, swzt(sub + r32, 2 * s + g));
+    fr.f[2 * s + 1] = lds_read_b128(buf + OFF_DO, swzt(sub + r32, 2 * s + g));
   }
 }
 
-// dV / dK block of one subtile: fragment 4 dt + 2 kt + 0 is dO^T, + 1 is Q^T,
-// head-dim rows 32 dt.., query chunk kt of the subtile.
-__device__ __forceinline__ void read_dvdk(const char* buf, int sub, int r32, int g, Frags& fr) {
+// dV / dK block of one subtile: fragment 4 dt + 2 kt + 0 is dO, + 1 is Q, as
+// B operands with head-dim columns 32 dt.. and the 16 query rows sub + 16 kt..
+__device__ __forceinline__ void read_dvdk(const char* buf, int sub, int lane, Frags& fr) {
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) {
-      const uint32_t off = swz128(32 * dt + r32, (sub >> 3) + 2 * kt + g);
-      fr.f[4 * dt + 2 * kt] = lds_read_b128(buf + OFF_DOT, off);
-      fr.f[4 * dt + 2 * kt + 1] = lds_read_b128(buf + OFF_QT, off);
+      fr.f[4 * dt + 2 * kt] = tr_operand(buf + OFF_DO, sub + 16 * kt, 32 * dt, lane);
+      fr.f[4 * dt + 2 * kt + 1] = tr_operand(buf + OFF_Q, sub + 16 * kt, 32 * dt, lane);
     }
 }
 
-// Scores of one subtile from its fragments, then P and dS (bf16 B operands).
+// Scores of one subtile from its fragments, then P and dS (bf16 A operands).
 template <bool CAUSAL>
 __device__ __forceinline__ void subtile_pds(const Frags& fr, const char* buf, int sub, uint32_t qs,
                                             uint32_t mykey, bool diag, int g,
@@ -148,11 +144,37 @@ __device__ __forceinline__ void dvdk_products(const Frags& fr, const bf16x8 (&pf
     }
 }
 
+// One pair of subtiles (rows base..base+63 of the tile).  The first subtile
+// of the pair is computed even where only the second is needed: the diagonal
+// mask then zeroes all of its P and dS.  Each block of 16 MFMAs finds its LDS
+// fragments already read: the reads of the next block are issued before the
+// products of the current one.
+template <bool CAUSAL>
+__device__ __forceinline__ void pair_step(const char* buf, int base, uint32_t qb, uint32_t kw,
+                                          uint32_t mykey, int r32, int g, int lane,
+                                          const bf16x8 (&kf)[8], const bf16x8 (&vf)[8],
+                                          f32x16 (&dva)[4], f32x16 (&dka)[4]) {
+  Frags fa, fb;
+  bf16x8 pf1[2], sf1[2], pf0[2], sf0[2];
+  const uint32_t q1 = qb + base + 32, q0 = qb + base;
+  read_sdp(buf, base + 32, r32, g, fa);
+  read_sdp(buf, base, r32, g, fb);
+  __builtin_amdgcn_sched_barrier(0);
+  subtile_pds<CAUSAL>(fa, buf, base + 32, q1, mykey, q1 < kw + 31, g, kf, vf, pf1, sf1);
+  read_dvdk(buf, base, lane, fa);
+  __builtin_amdgcn_sched_barrier(0);
+  subtile_pds<CAUSAL>(fb, buf, base, q0, mykey, q0 < kw + 31, g, kf, vf, pf0, sf0);
+  read_dvdk(buf, base + 32, lane, fb);
+  __builtin_amdgcn_sched_barrier(0);
+  dvdk_products(fa, pf0, sf0, dva, dka);
+  dvdk_products(fb, pf1, sf1, dva, dka);
+}
+
 template <bool CAUSAL>
 __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(
-    const bf16* __restrict__ Qc, const bf16* __restrict__ Qct, const bf16* __restrict__ dOc,
-    const bf16* __restrict__ dOct, const float* __restrict__ lse_c, const float* __restrict__ Dc,
-    const bf16* __restrict__ Kp, const bf16* __restrict__ Vp, float* __restrict__ dK32,
+    const bf16* __restrict__ Qc, const bf16* __restrict__ dOc, const float* __restrict__ lse_c,
+    const float* __restrict__ Dc, const bf16* __restrict__ Kp, const bf16* __restrict__ Vp,
+    float* __restrict__ dK32,
     float* __restrict__ dV32, bf16* __restrict__ dk, bf16* __restrict__ dv, int64_t S, int64_t Sp,
     int U, int h0, int G, int Hkv) {
   __shared__ __attribute__((aligned(1024))) char smem[2 * KV_STAGE];
@@ -168,27 +190,23 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(
   const int hlo = max(h0, kvh * G), hhi = min(h0 + U, (kvh + 1) * G);
   const bool first = kvh * G >= h0;           // no earlier chunk touched kvh
   const bool last = (kvh + 1) * G <= h0 + U;  // no later chunk will
-  const uint32_t nqt = Spv / QT;
+  const uint32_t nqt = (Spv + QT - 1) / QT;
   const uint32_t qt_lo = CAUSAL ? kb0 / QT : 0;   // lowest query tile needed
   const uint32_t per_head = nqt - qt_lo;
   const int total = (int)(per_head * (hhi - hlo));
 
-  uint32_t offr[4], offc[4];
+  uint32_t offr[KV_BLK];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int blk = 4 * w + i;
+  for (int i = 0; i < KV_BLK; ++i) {
+    const int blk = KV_BLK * w + i;
     const int r = 4 * blk + (lane >> 4);      // Q / dO row of the tile, 16 lanes per row
-    offr[i] = r * 256u + (((lane & 15) ^ (r & 15)) << 4);
-    const int c = 8 * blk + (lane >> 3);      // Q^T / dO^T row (head-dim), 8 lanes per row
-    offc[i] = c * (Spv * 2u) + (((lane & 7) ^ (c & 7) ^ ((c >> 3) & 1)) << 4);
+    offr[i] = r * 256u + (((lane & 15) ^ tsw(r)) << 4);
   }
   auto srcs = [&](int hh) {
     QStageSrc r;
     const int64_t hoff = (int64_t)(hh - h0) * Sp * HEAD_DIM;
     r.q = make_rsrc(Qc + hoff, Spv * 256u);
     r.dO = make_rsrc(dOc + hoff, Spv * 256u);
-    r.qt = make_rsrc(Qct + hoff, Spv * 256u);
-    r.dOt = make_rsrc(dOct + hoff, Spv * 256u);
     r.lse = make_rsrc(lse_c + (int64_t)(hh - h0) * Sp, Spv * 4u);
     r.D = make_rsrc(Dc + (int64_t)(hh - h0) * Sp, Spv * 4u);
     return r;
@@ -196,7 +214,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(
 
   // First tile: head hlo, query tile nqt-1.
   QStageSrc cur = srcs(hlo);
-  issue_qstage(cur, offr, offc, (nqt - 1) * QT, smem, w, lane);
+  issue_qstage(cur, offr, (nqt - 1) * QT, smem, w, lane);
 
   // K and V B-operand fragments (lane = key column, k = head dim).
   bf16x8 kf[8], vf[8];
@@ -250,28 +268,15 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(
     __syncthreads();   // this tile landed for all waves; the other buffer is free
     if (it + 1 < total) {
       if (nh != hh) cur = srcs(nh);
-      issue_qstage(cur, offr, offc, nq * QT, smem + ((it + 1) & 1) * KV_STAGE, w, lane);
+      issue_qstage(cur, offr, nq * QT, smem + ((it + 1) & 1) * KV_STAGE, w, lane);
     }
-
-    // Causal: a tile is needed when its last row reaches this wave's first
-    // key; on the one tile where only its second subtile does, the first is
-    // computed under the diagonal mask, which zeroes all of its P and dS.
-    // Each block of 16 MFMAs finds its LDS fragments already read: the reads
-    // of the next block are issued before the products of the current one.
-    if (!CAUSAL || qb + 63 >= kw) {
-      Frags fa, fb;
-      bf16x8 pf1[2], sf1[2], pf0[2], sf0[2];
-      read_sdp(buf, 32, r32, g, fa);
-      read_sdp(buf, 0, r32, g, fb);
-      __builtin_amdgcn_sched_barrier(0);
-      subtile_pds<CAUSAL>(fa, buf, 32, qb + 32, mykey, qb + 32 < kw + 31, g, kf, vf, pf1, sf1);
-      read_dvdk(buf, 0, r32, g, fa);
-      __builtin_amdgcn_sched_barrier(0);
-      subtile_pds<CAUSAL>(fb, buf, 0, qb, mykey, qb < kw + 31, g, kf, vf, pf0, sf0);
-      read_dvdk(buf, 32, r32, g, fb);
-      __builtin_amdgcn_sched_barrier(0);
-      dvdk_products(fa, pf0, sf0, dva, dka);
-      dvdk_products(fb, pf1, sf1, dva, dka);
+    // Pairs of 32-row subtiles, upper rows first; a pair is needed when its
+    // last row reaches this wave's first key (and lies inside the sequence).
+#pragma unroll
+    for (int pp = QT / 64 - 1; pp >= 0; --pp) {
+      const uint32_t pb = qb + 64 * pp;
+      if (pb < Spv && (!CAUSAL || pb + 63 >= kw))
+        pair_step<CAUSAL>(buf, 64 * pp, qb, kw, mykey, r32, g, lane, kf, vf, dva, dka);
     }
     qt = nq;
     hh = nh;
@@ -303,34 +308,34 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(
 
 // ---------------------------------------------------------------------- dQ
 // Workgroup = 8 waves x 32 query rows (256 rows, two waves per SIMD).  LDS
-// stage for one 64-key tile: K [64][128], V [64][128] (256-B rows) and K^T
-// [128][64] in MFMA order (128-B rows); a stage is consumed as two 32-key
-// subtiles, keys ascending.
+// stage for one tile of DQ_BK keys: K and V rows [DQ_BK][128] (256-B rows).
+// The A operand of dQ^T = K^T . dS^T is read out of the K rows with
+// transposing LDS reads, so no [d][S] copy of K is needed.
 constexpr int DQ_BQ = 256;
 constexpr int DQ_BK = 64;
-constexpr int DQ_T = DQ_BK * HEAD_DIM * 2;   // 16 KB
-constexpr int DQ_OFF_K = 0, DQ_OFF_V = DQ_T, DQ_OFF_KT = 2 * DQ_T;
-constexpr int DQ_STAGE = 3 * DQ_T;
+constexpr int DQ_T = DQ_BK * HEAD_DIM * 2;
+constexpr int DQ_OFF_K = 0, DQ_OFF_V = DQ_T;
+constexpr int DQ_STAGE = 2 * DQ_T;
+constexpr int DQ_BLK = DQ_T / 1024 / 8;   // 1 KB blocks per wave per tile
 
-// This wave's share of one stage's copies: 2 blocks of 1 KB each of K rows,
-// V rows (4 rows of 256 B) and K^T rows (8 rows of 128 B).
-__device__ __forceinline__ void issue_kstage(buf_rsrc rk, buf_rsrc rv, buf_rsrc rkt,
-                                             const uint32_t (&offr)[2], const uint32_t (&offt)[2],
-                                             uint32_t kb, char* buf, int w) {
+// This wave's share of one tile's copies: DQ_BLK blocks of 1 KB each of K
+// rows (transposing-read swizzle) and V rows (4 rows of 256 B per block).
+__device__ __forceinline__ void issue_kstage(buf_rsrc rk, buf_rsrc rv, const uint32_t (&offk)[DQ_BLK],
+                                             const uint32_t (&offv)[DQ_BLK], uint32_t kb, char* buf,
+                                             int w) {
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int blk = 2 * w + i;
-    dma_buf_b128(rk, offr[i], kb * 256u, buf + DQ_OFF_K + blk * 1024);
-    dma_buf_b128(rv, offr[i], kb * 256u, buf + DQ_OFF_V + blk * 1024);
-    dma_buf_b128(rkt, offt[i], kb * 2u, buf + DQ_OFF_KT + blk * 1024);
+  for (int i = 0; i < DQ_BLK; ++i) {
+    const int blk = DQ_BLK * w + i;
+    dma_buf_b128(rk, offk[i], kb * 256u, buf + DQ_OFF_K + blk * 1024);
+    dma_buf_b128(rv, offv[i], kb * 256u, buf + DQ_OFF_V + blk * 1024);
   }
 }
 
 template <bool CAUSAL>
 __global__ __launch_bounds__(512, 1) void attn_bwd_dq_kernel(
     const bf16* __restrict__ Qc, const bf16* __restrict__ dOc, const float* __restrict__ lse_c,
-    const float* __restrict__ Dc, const bf16* __restrict__ Kp, const bf16* __restrict__ Kt,
-    const bf16* __restrict__ Vp, bf16* __restrict__ dQc, int64_t S, int64_t Sp, int U, int h0,
+    const float* __restrict__ Dc, const bf16* __restrict__ Kp, const bf16* __restrict__ Vp,
+    bf16* __restrict__ dQc, int64_t S, int64_t Sp, int U, int h0,
     int G, int nqb) {
   __shared__ __attribute__((aligned(1024))) char smem[2 * DQ_STAGE];
   const int t = threadIdx.x;
@@ -348,21 +353,19 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_kernel(
   const uint32_t Sv = (uint32_t)S;
   const bool rows_ok = qw < Spv;            // the last block may hold 128 rows only
 
-  // One head's K and V rows [Sp][128] and K^T rows [128][Sp], 32-bit addressed.
+  // One head's K and V rows [Sp][128], 32-bit addressed.
   const buf_rsrc rk = make_rsrc(Kp + (int64_t)kvh * Sp * HEAD_DIM, Spv * 256u);
   const buf_rsrc rv = make_rsrc(Vp + (int64_t)kvh * Sp * HEAD_DIM, Spv * 256u);
-  const buf_rsrc rkt = make_rsrc(Kt + (int64_t)kvh * HEAD_DIM * Sp, Spv * 256u);
-  uint32_t offr[2], offt[2];
+  uint32_t offk[DQ_BLK], offv[DQ_BLK];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int blk = 2 * w + i;
-    const int r = 4 * blk + (lane >> 4);      // K/V row of the stage, 16 lanes per row
-    offr[i] = r * 256u + (((lane & 15) ^ (r & 15)) << 4);
-    const int c = 8 * blk + (lane >> 3);      // K^T row (head-dim), 8 lanes per row
-    offt[i] = c * (Spv * 2u) + (((lane & 7) ^ (c & 7) ^ ((c >> 3) & 1)) << 4);
+  for (int i = 0; i < DQ_BLK; ++i) {
+    const int blk = DQ_BLK * w + i;
+    const int r = 4 * blk + (lane >> 4);      // row of the tile, 16 lanes per row
+    offk[i] = r * 256u + (((lane & 15) ^ tsw(r)) << 4);
+    offv[i] = r * 256u + (((lane & 15) ^ (r & 15)) << 4);
   }
-  const int nst = CAUSAL ? (int)(min(q0 + DQ_BQ, Spv) / DQ_BK) : (int)(Spv / DQ_BK);
-  issue_kstage(rk, rv, rkt, offr, offt, 0, smem, w);
+  const int nst = CAUSAL ? (int)((min(q0 + DQ_BQ, Spv) + DQ_BK - 1) / DQ_BK) : (int)(Spv / DQ_BK);
+  issue_kstage(rk, rv, offk, offv, 0, smem, w);
 
   bf16x8 qf[8], df[8];
   float lse2 = 0.f, Dq = 0.f;
@@ -391,47 +394,51 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_kernel(
     const uint32_t ks = (uint32_t)j * DQ_BK;
     char* buf = smem + (j & 1) * DQ_STAGE;
     wait_vmem();
-    __syncthreads();   // stage j landed for all waves; stage j-1's buffer is free
-    if (j + 1 < nst) issue_kstage(rk, rv, rkt, offr, offt, ks + DQ_BK, smem + ((j + 1) & 1) * DQ_STAGE, w);
+    __syncthreads();   // tile j landed for all waves; tile j-1's buffer is free
+    if (j + 1 < nst) issue_kstage(rk, rv, offk, offv, ks + DQ_BK, smem + ((j + 1) & 1) * DQ_STAGE, w);
     if (!rows_ok) continue;
-    if (CAUSAL && ks > qw + 31) continue;    // whole stage masked for this wave
-    f32x16 sacc[2], pacc[2];
 #pragma unroll
-    for (int hh = 0; hh < 2; ++hh)
+    for (int h64 = 0; h64 < DQ_BK / 64; ++h64) {
+      const uint32_t kb = ks + 64 * h64;
+      if (CAUSAL && kb > qw + 31) break;     // rest of the tile masked for this wave
+      f32x16 sacc[2], pacc[2];
 #pragma unroll
-      for (int i = 0; i < 16; ++i) { sacc[hh][i] = 0.f; pacc[hh][i] = 0.f; }
+      for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
-    for (int s = 0; s < 8; ++s)
+        for (int i = 0; i < 16; ++i) { sacc[hh][i] = 0.f; pacc[hh][i] = 0.f; }
+#pragma unroll
+      for (int s = 0; s < 8; ++s)
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          const int row = 64 * h64 + 32 * hh + r32;
+          sacc[hh] = mfma32x32x16(lds_read_b128(buf + DQ_OFF_K, swzt(row, 2 * s + g)), qf[s], sacc[hh]);
+          pacc[hh] = mfma32x32x16(lds_read_b128(buf + DQ_OFF_V, swz256(row, 2 * s + g)), df[s], pacc[hh]);
+        }
+      const bool diag = CAUSAL ? (kb + 63 > qw) : (kb + 64 > Sv);
+      bf16x8 sf[2][2];
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh) {
-        const int row = 32 * hh + r32;
-        sacc[hh] = mfma32x32x16(lds_read_b128(buf + DQ_OFF_K, swz256(row, 2 * s + g)), qf[s], sacc[hh]);
-        pacc[hh] = mfma32x32x16(lds_read_b128(buf + DQ_OFF_V, swz256(row, 2 * s + g)), df[s], pacc[hh]);
-      }
-    const bool diag = CAUSAL ? (ks + DQ_BK - 1 > qw) : (ks + DQ_BK > Sv);
-    bf16x8 sf[2][2];
+        float p[16];
 #pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-      float p[16];
+        for (int i = 0; i < 16; ++i) p[i] = fast_exp2(fmaf(sacc[hh][i], kSl2, -lse2));
+        if (diag) {   // wave-uniform
 #pragma unroll
-      for (int i = 0; i < 16; ++i) p[i] = fast_exp2(fmaf(sacc[hh][i], kSl2, -lse2));
-      if (diag) {   // wave-uniform
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const uint32_t key = ks + 32 * hh + 8 * (i >> 2) + 4 * g + (i & 3);
-          const bool vis = CAUSAL ? (key <= myq) : (key < Sv);
-          if (!vis) p[i] = 0.f;
+          for (int i = 0; i < 16; ++i) {
+            const uint32_t key = kb + 32 * hh + 8 * (i >> 2) + 4 * g + (i & 3);
+            const bool vis = CAUSAL ? (key <= myq) : (key < Sv);
+            if (!vis) p[i] = 0.f;
+          }
         }
+#pragma unroll
+        for (int i = 0; i < 16; ++i) sf[hh][i >> 3][i & 7] = (bf16)(p[i] * (pacc[hh][i] - Dq));
       }
 #pragma unroll
-      for (int i = 0; i < 16; ++i) sf[hh][i >> 3][i & 7] = (bf16)(p[i] * (pacc[hh][i] - Dq));
+      for (int c = 0; c < 4; ++c)
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt)
+          qacc[dt] = mfma32x32x16(tr_operand(buf + DQ_OFF_K, 64 * h64 + 16 * c, 32 * dt, lane),
+                                  sf[c >> 1][c & 1], qacc[dt]);
     }
-#pragma unroll
-    for (int c = 0; c < 4; ++c)
-#pragma unroll
-      for (int dt = 0; dt < 4; ++dt)
-        qacc[dt] = mfma32x32x16(lds_read_b128(buf + DQ_OFF_KT, swz128(32 * dt + r32, 2 * c + g)),
-                                sf[c >> 1][c & 1], qacc[dt]);
   }
 
   if (!rows_ok) return;
@@ -449,33 +456,32 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_kernel(
 
 }  // namespace
 
-hipError_t launch_attn_bwd_dkdv(const bf16* Qc, const bf16* Qct, const bf16* dOc,
-                                const bf16* dOct, const float* lse_c, const float* D,
+hipError_t launch_attn_bwd_dkdv(const bf16* Qc, const bf16* dOc, const float* lse_c, const float* D,
                                 const bf16* Kp, const bf16* Vp, float* dK32, float* dV32, bf16* dk,
                                 bf16* dv, int64_t S, int64_t Sp, int U, int h0, int G, int Hkv,
                                 int causal, hipStream_t st) {
   const int kv_lo = h0 / G, kv_hi = (h0 + U - 1) / G;
   dim3 grid((unsigned)(Sp / 128), (unsigned)(kv_hi - kv_lo + 1));
   if (causal)
-    hipLaunchKernelGGL(attn_bwd_dkdv_kernel<true>, grid, dim3(256), 0, st, Qc, Qct, dOc, dOct,
-                       lse_c, D, Kp, Vp, dK32, dV32, dk, dv, S, Sp, U, h0, G, Hkv);
+    hipLaunchKernelGGL(attn_bwd_dkdv_kernel<true>, grid, dim3(256), 0, st, Qc, dOc, lse_c, D, Kp,
+                       Vp, dK32, dV32, dk, dv, S, Sp, U, h0, G, Hkv);
   else
-    hipLaunchKernelGGL(attn_bwd_dkdv_kernel<false>, grid, dim3(256), 0, st, Qc, Qct, dOc, dOct,
-                       lse_c, D, Kp, Vp, dK32, dV32, dk, dv, S, Sp, U, h0, G, Hkv);
+    hipLaunchKernelGGL(attn_bwd_dkdv_kernel<false>, grid, dim3(256), 0, st, Qc, dOc, lse_c, D, Kp,
+                       Vp, dK32, dV32, dk, dv, S, Sp, U, h0, G, Hkv);
   return hipGetLastError();
 }
 
 hipError_t launch_attn_bwd_dq(const bf16* Qc, const bf16* dOc, const float* lse_c, const float* D,
-                              const bf16* Kp, const bf16* Kt, const bf16* Vp, bf16* dQc, int64_t S,
-                              int64_t Sp, int U, int h0, int G, int causal, hipStream_t st) {
+                              const bf16* Kp, const bf16* Vp, bf16* dQc, int64_t S, int64_t Sp,
+                              int U, int h0, int G, int causal, hipStream_t st) {
   const int nqb = (int)((Sp + DQ_BQ - 1) / DQ_BQ);
   dim3 grid((unsigned)(nqb * U));
   if (causal)
-    hipLaunchKernelGGL(attn_bwd_dq_kernel<true>, grid, dim3(512), 0, st, Qc, dOc, lse_c, D, Kp, Kt,
-                       Vp, dQc, S, Sp, U, h0, G, nqb);
+    hipLaunchKernelGGL(attn_bwd_dq_kernel<true>, grid, dim3(512), 0, st, Qc, dOc, lse_c, D, Kp, Vp,
+                       dQc, S, Sp, U, h0, G, nqb);
   else
     hipLaunchKernelGGL(attn_bwd_dq_kernel<false>, grid, dim3(512), 0, st, Qc, dOc, lse_c, D, Kp,
-                       Kt, Vp, dQc, S, Sp, U, h0, G, nqb);
+                       Vp, dQc, S, Sp, U, h0, G, nqb);
   return hipGetLastError();
 }
 

@@ -9,16 +9,17 @@
 // Work decomposition
 //   workgroup = 8 waves x 32 query rows = one 256-row query block of one head
 //               (two waves per SIMD, one workgroup per CU)
-//   key stage = 128 keys, double-buffered in LDS (K rows 32 KB, V^T 32 KB),
+//   key stage = 128 keys, double-buffered in LDS (K rows 32 KB, V rows 32 KB),
 //               filled by buffer->LDS copies issued one stage ahead
 //   per wave per stage: S^T = K . Q^T    (4 x 8 MFMA 32x32x16, keys on rows)
 //                       O^T += V^T . P^T (8 x 4 MFMA)
 // Computing S^T (keys x queries) puts one query column in each lane: the
 // scores of a row sit in one lane pair, and the C tile converts in registers
-// into the B operand of the P.V product (V^T is stored in MFMA order, see
-// common.h).  A stage of 128 keys per barrier halves the copies and barriers
-// per product against 64-key tiles, and 256 rows per workgroup halve the
-// L2->LDS traffic per query.
+// into the B operand of the P.V product, whose V^T operand is read out of
+// the V rows with transposing LDS reads (tr_operand, common.h).  A stage of
+// 128 keys per barrier halves the copies and barriers per product against
+// 64-key tiles, and 256 rows per workgroup halve the L2->LDS traffic per
+// query.
 //
 // Lazy rescaling: probabilities are taken against a reference max m_ref that
 // moves only when needed.  A lane's sum of its stage probabilities bounds
@@ -42,14 +43,15 @@ constexpr int STAGE = K_TILE + V_TILE;
 constexpr float kSumMax = 256.f;   // lazy-rescale bound on a lane's stage sum (2^8)
 
 // This wave's share of the copies of the 128-key stage at `kb`: 4 blocks of
-// 1 KB of K rows and 4 of V^T rows (4 rows of 256 B each).  The lane offsets
+// 1 KB of K rows and 4 of V rows (4 rows of 256 B each, V in the swizzle of
+// transposing reads).  The lane offsets
 // inside a stage are fixed; the stage offset is uniform.
 __device__ __forceinline__ void issue_tile(buf_rsrc rk, buf_rsrc rv, const uint32_t (&offk)[4],
                                            const uint32_t (&offv)[4], uint32_t kb, char* buf, int w) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) dma_buf_b128(rk, offk[i], kb * 256u, buf + (4 * w + i) * 1024);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) dma_buf_b128(rv, offv[i], kb * 2u, buf + K_TILE + (4 * w + i) * 1024);
+  for (int i = 0; i < 4; ++i) dma_buf_b128(rv, offv[i], kb * 256u, buf + K_TILE + (4 * w + i) * 1024);
 }
 
 __device__ __forceinline__ float tile_probs4(const f32x16 (&st)[4], bf16x8 (&pf)[4][2], float m_ref,
@@ -72,7 +74,7 @@ __device__ __forceinline__ float tile_probs4(const f32x16 (&st)[4], bf16x8 (&pf)
 
 template <bool CAUSAL>
 __global__ __launch_bounds__(512, 1) void attn_fwd_kernel(
-    const bf16* __restrict__ Qc, const bf16* __restrict__ Kp, const bf16* __restrict__ Vt,
+    const bf16* __restrict__ Qc, const bf16* __restrict__ Kp, const bf16* __restrict__ Vp,
     bf16* __restrict__ Oc, float* __restrict__ lse, int64_t S, int64_t Sp, int U, int h0, int G,
     int nqb) {
   __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
@@ -91,9 +93,9 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_kernel(
   const uint32_t Sv = (uint32_t)S;
   const bool rows_ok = qw < Spv;            // the last block may hold 128 rows only
 
-  // One head's K rows [Sp][128] and V^T rows [128][Sp], 32-bit addressed.
+  // One head's K and V rows [Sp][128], 32-bit addressed.
   const buf_rsrc rk = make_rsrc(Kp + (int64_t)kvh * Sp * HEAD_DIM, Spv * 256u);
-  const buf_rsrc rv = make_rsrc(Vt + (int64_t)kvh * HEAD_DIM * Sp, Spv * 256u);
+  const buf_rsrc rv = make_rsrc(Vp + (int64_t)kvh * Sp * HEAD_DIM, Spv * 256u);
   uint32_t offk[4], offv[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -101,7 +103,7 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_kernel(
     const int r = 4 * blk + (lane >> 4);       // stage row, 16 lanes per row
     const uint32_t c = (uint32_t)((lane & 15) ^ (r & 15)) << 4;
     offk[i] = r * 256u + c;
-    offv[i] = r * (Spv * 2u) + c;
+    offv[i] = r * 256u + (((lane & 15) ^ tsw(r)) << 4);
   }
 
   const int nst = CAUSAL ? (int)(min(q0 + BQ, Spv) / BKS) : (int)(Spv / BKS);
@@ -185,8 +187,8 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_kernel(
       for (int c = 0; c < 8; ++c)
 #pragma unroll
         for (int dt = 0; dt < 4; ++dt)
-          oacc[dt] = mfma32x32x16(lds_read_b128(buf + K_TILE, swz256(32 * dt + r32, 2 * c + g)),
-                                  pf[c >> 1][c & 1], oacc[dt]);
+          oacc[dt] = mfma32x32x16(tr_operand(buf + K_TILE, 16 * c, 32 * dt, lane), pf[c >> 1][c & 1],
+                                  oacc[dt]);
     }
   }
 
@@ -209,16 +211,16 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_kernel(
 
 }  // namespace
 
-hipError_t launch_attn_fwd(const bf16* Qc, const bf16* Kp, const bf16* Vt, bf16* Oc, float* lse,
+hipError_t launch_attn_fwd(const bf16* Qc, const bf16* Kp, const bf16* Vp, bf16* Oc, float* lse,
                            int64_t S, int64_t Sp, int U, int h0, int G, int causal,
                            hipStream_t st) {
   const int nqb = (int)((Sp + BQ - 1) / BQ);
   dim3 grid((unsigned)(nqb * U));
   if (causal)
-    hipLaunchKernelGGL(attn_fwd_kernel<true>, grid, dim3(512), 0, st, Qc, Kp, Vt, Oc, lse, S, Sp,
+    hipLaunchKernelGGL(attn_fwd_kernel<true>, grid, dim3(512), 0, st, Qc, Kp, Vp, Oc, lse, S, Sp,
                        U, h0, G, nqb);
   else
-    hipLaunchKernelGGL(attn_fwd_kernel<false>, grid, dim3(512), 0, st, Qc, Kp, Vt, Oc, lse, S, Sp,
+    hipLaunchKernelGGL(attn_fwd_kernel<false>, grid, dim3(512), 0, st, Qc, Kp, Vp, Oc, lse, S, Sp,
                        U, h0, G, nqb);
   return hipGetLastError();
 }

@@ -10,12 +10,9 @@
 //   C/D:       lane l holds column (l % 32); element i of its 16 floats is
 //              row 8*(i/4) + 4*g + (i%4).
 //
-// "MFMA order" of a transposed copy: a buffer stored [d][S] (sequence index
-// contiguous) keeps, inside every aligned block of 16 positions, the element
-// of sequence index perm16(p) at position p, where perm16 swaps bits 2 and 3.
-// Then the 16 floats one lane holds in a C tile (rows 8a+4g+b) become, after
-// conversion to bf16, exactly the B/A-operand vectors that read 8 consecutive
-// positions 16*kt + 8*g + j of such a buffer.  perm16 is an involution.
+// Transposed operands (V^T, K^T, Q^T, dO^T) are never stored: they are read
+// out of the row-major [S][128] tiles in LDS with ds_read_b64_tr_b16 (see
+// tr_operand), which hands each lane one column of a 4-row block.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -32,10 +29,6 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int HEAD_DIM = 128;   // the only supported head width
 constexpr int SEQ_PAD = 128;    // sequence padding granule of packed buffers
-
-__host__ __device__ inline int64_t perm16(int64_t p) {
-  return (p & ~int64_t(12)) | ((p & 4) << 1) | ((p & 8) >> 1);
-}
 
 __host__ __device__ inline int64_t round_up(int64_t x, int64_t m) {
   return (x + m - 1) / m * m;
@@ -83,18 +76,42 @@ __device__ __forceinline__ void dma_buf_b128(buf_rsrc r, uint32_t voff, uint32_t
 // Wait until every outstanding global load of this wave has completed.
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x3F70); }
 
-// 16-byte chunk swizzles.  Rows of 256 B (16 chunks): chunk c of row r is
-// stored at c ^ (r & 15).  Rows of 128 B (8 chunks): c ^ (r & 7) ^ ((r>>3) & 1).
-// Rows of 64 B (4 chunks): c ^ ((r >> 1) & 3).  For the MFMA operand reads
-// (consecutive lanes = consecutive rows, same logical chunk) these are free of
-// bank conflicts for both 32- and 64-bank LDS.
+// 16-byte chunk swizzles of 256-B rows (16 chunks).  swz256: chunk c of row
+// r at c ^ (r & 15).  swzt: chunk c of row r at c ^ tsw(r), where tsw swaps
+// the two 2-bit halves of r mod 16.  Both put the sixteen consecutive rows of
+// a plain MFMA operand read (same logical chunk) in sixteen distinct slots;
+// swzt also spreads the 8 rows x 4 chunks of a transposing read (tr_operand)
+// over every slot exactly twice, the minimum for its 512 bytes.
 __device__ __forceinline__ uint32_t swz256(int r, int c) { return r * 256 + ((c ^ (r & 15)) << 4); }
-__device__ __forceinline__ uint32_t swz128(int r, int c) {
-  return r * 128 + ((c ^ (r & 7) ^ ((r >> 3) & 1)) << 4);
+__device__ __forceinline__ uint32_t tsw(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
+__device__ __forceinline__ uint32_t swzt(int r, int c) { return r * 256 + ((c ^ tsw(r)) << 4); }
+
+// MFMA operand whose k index runs down the rows of a row-major [k][n] tile of
+// 256-B rows stored with swzt (A and B operands have the same lane layout):
+// lane l gets column n0 + (l % 32) at rows k0 + 4g + {0..3} (elements 0..3)
+// and k0 + 8 + 4g + {0..3} (elements 4..7), g = l / 32 -- the k order in
+// which a lane holds the rows of a C tile (rows 8a + 4g + b), so P and dS
+// fragments taken from C tiles pair with it directly.  ds_read_b64_tr_b16:
+// within each 16-lane group, loader lane t reads the 8 bytes at row
+// k0 + 4g + t/4, columns n0 + 16 * ((l >> 4) & 1) + 4 (t % 4), and receiver
+// lane t gets column t of the group's 16 columns for those four rows.
+__device__ __forceinline__ bf16x8 tr_operand(const char* tile, int k0, int n0, int lane) {
+  typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+  const int t = lane & 15, hi = (lane >> 4) & 1, g = lane >> 5;
+  const int col = n0 + 16 * hi + 4 * (t & 3);
+  const int r0 = k0 + 4 * g + (t >> 2);
+  const uint32_t cb = (uint32_t)(col & 7) << 1;   // byte offset inside the 16-byte chunk
+  const bf16x4 lo =
+      __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(tile + swzt(r0, col >> 3) + cb));
+  const bf16x4 up =
+      __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(tile + swzt(r0 + 8, col >> 3) + cb));
+  bf16x8 v;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    v[e] = lo[e];
+    v[4 + e] = up[e];
+  }
+  return v;
 }
-__device__ __forceinline__ uint32_t swz64(int r, int c) { return r * 64 + ((c ^ ((r >> 1) & 3)) << 4); }
-// Rows of 64 B for 64-bank LDS (measured on gfx950): c ^ ((r >> 2) & 3) puts
-// the 16 rows read together in 16 distinct 16-byte bank groups.
-__device__ __forceinline__ uint32_t swz64b(int r, int c) { return r * 64 + ((c ^ ((r >> 2) & 3)) << 4); }
 
 }  // namespace upipe

@@ -34,11 +34,9 @@ enum { GEMM_EPI_HEADS = 0, GEMM_EPI_ACC32 = 1, GEMM_EPI_PARTIAL = 2 };
 
 struct GemmEpilogue {
   // GEMM_EPI_HEADS: output column block nb (128 wide) is head nb of group 0
-  // if nb < n_split, else head nb - n_split of group 1.  dst_norm[g] is
-  // [heads][Sp][128], dst_t[g] is [heads][128][Sp] in MFMA order; either may
-  // be null.  Every row m < M is written.
+  // if nb < n_split, else head nb - n_split of group 1; dst_norm[g] is
+  // [heads][Sp][128].  Every row m < M is written.
   bf16* dst_norm[2];
-  bf16* dst_t[2];
   int64_t n_split;
   int64_t Sp;
   // GEMM_EPI_ACC32: accumulators start at c32[m][n] (ldc) unless `first`;

@@ -195,22 +195,10 @@ __global__ __launch_bounds__(256, 2) void gemm_kernel(GemmOperand A, GemmOperand
         const int grp = nb < E.n_split ? 0 : 1;
         const int64_t head = nb - (grp ? E.n_split : 0);
         bf16* dn = E.dst_norm[grp];
-        bf16* dt = E.dst_t[grp];
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const int64_t m = mb + 8 * (i >> 2) + 4 * g + (i & 3);
-          if (dn) dn[(head * E.Sp + m) * 128 + e] = (bf16)acc[mt][nt][i];
-        }
-        if (dt) {
-          // Rows 16kt + 8a' + 4g + b sit at MFMA-order positions
-          // 16kt + 8g + 4a' + b: eight consecutive positions per kt.
-#pragma unroll
-          for (int kt = 0; kt < 2; ++kt) {
-            bf16x8 v8;
-#pragma unroll
-            for (int j = 0; j < 8; ++j) v8[j] = (bf16)acc[mt][nt][8 * kt + j];
-            *reinterpret_cast<bf16x8*>(dt + (head * 128 + e) * E.Sp + mb + 16 * kt + 8 * g) = v8;
-          }
+          dn[(head * E.Sp + m) * 128 + e] = (bf16)acc[mt][nt][i];
         }
       } else if (EPI == GEMM_EPI_ACC32) {
 #pragma unroll

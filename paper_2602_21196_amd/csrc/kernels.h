@@ -10,10 +10,9 @@
 namespace upipe {
 
 // ---- layout (layout.hip) -------------------------------------------------
-// src [S, H, d] heads h0..h0+n-1  ->  dst [n, Sp, d] and/or dst_t [n, d, Sp]
-// (MFMA order); rows >= S are zero.  Either destination may be null.
+// src [S, H, d] heads h0..h0+n-1  ->  dst [n, Sp, d]; rows >= S are zero.
 hipError_t launch_pack_rows(const bf16* src, int64_t S, int H, int h0, int n,
-                            int64_t Sp, bf16* dst, bf16* dst_t, hipStream_t st);
+                            int64_t Sp, bf16* dst, hipStream_t st);
 // src [n, Sp, d] rows < S  ->  dst [S, H, d] heads h0..h0+n-1.
 hipError_t launch_unpack_rows(const bf16* src, int64_t S, int H, int h0, int n,
                               int64_t Sp, bf16* dst, hipStream_t st);
@@ -27,9 +26,9 @@ hipError_t launch_rowdot_lse(const bf16* a, int64_t a_row, int64_t a_head,
                              hipStream_t st);
 
 // ---- attention forward (attn_fwd.hip) ------------------------------------
-// Qc [U, Sp, d], Kp [Hkv, Sp, d], Vt [Hkv, d, Sp] (MFMA order) -> Oc [U, Sp, d]
-// and lse rows h0..h0+U-1 of the caller's [Hq, S] array.
-hipError_t launch_attn_fwd(const bf16* Qc, const bf16* Kp, const bf16* Vt,
+// Qc [U, Sp, d], Kp and Vp [Hkv, Sp, d] -> Oc [U, Sp, d] and lse rows
+// h0..h0+U-1 of the caller's [Hq, S] array.
+hipError_t launch_attn_fwd(const bf16* Qc, const bf16* Kp, const bf16* Vp,
                            bf16* Oc, float* lse, int64_t S, int64_t Sp, int U,
                            int h0, int G, int causal, hipStream_t st);
 
@@ -39,8 +38,7 @@ hipError_t launch_attn_fwd(const bf16* Qc, const bf16* Kp, const bf16* Vt,
 // dK32/dV32 [Hkv, Sp, d] (read unless the chunk holds a group's first head),
 // written back there, or -- when the chunk holds the group's last head --
 // scaled and rounded into dk/dv bf16 [S, Hkv, d].
-hipError_t launch_attn_bwd_dkdv(const bf16* Qc, const bf16* Qct,
-                                const bf16* dOc, const bf16* dOct,
+hipError_t launch_attn_bwd_dkdv(const bf16* Qc, const bf16* dOc,
                                 const float* lse_c, const float* D,
                                 const bf16* Kp, const bf16* Vp, float* dK32,
                                 float* dV32, bf16* dk, bf16* dv, int64_t S,
@@ -49,8 +47,7 @@ hipError_t launch_attn_bwd_dkdv(const bf16* Qc, const bf16* Qct,
 // dQc [U, Sp, d] of the chunk's heads.
 hipError_t launch_attn_bwd_dq(const bf16* Qc, const bf16* dOc,
                               const float* lse_c, const float* D,
-                              const bf16* Kp, const bf16* Kt, const bf16* Vp,
-                              bf16* dQc, int64_t S, int64_t Sp, int U, int h0,
+                              const bf16* Kp, const bf16* Vp, bf16* dQc, int64_t S, int64_t Sp, int U, int h0,
                               int G, int causal, hipStream_t st);
 
 }  // namespace upipe

@@ -54,7 +54,7 @@ int64_t wgrad_split_len(int64_t S) {
 
 struct LayerFwdPlan {
   int64_t Sp = 0;
-  size_t Kp = 0, Vt = 0, Qc = 0, Oc = 0, Y32 = 0, total = 0;
+  size_t Kp = 0, Vp = 0, Qc = 0, Oc = 0, Y32 = 0, total = 0;
   bool y32 = false;
 };
 
@@ -71,7 +71,7 @@ LayerFwdPlan plan_layer_fwd(int64_t S, int d_model, int Hq, int Hkv, int U) {
   const size_t head = (size_t)p.Sp * HEAD_DIM * 2;
   Carver c;
   p.Kp = c.take(Hkv * head);
-  p.Vt = c.take(Hkv * head);
+  p.Vp = c.take(Hkv * head);
   p.Qc = c.take(U * head);
   p.Oc = c.take(U * head);
   p.y32 = Hq / U > 1;
@@ -97,12 +97,10 @@ LayerBwdPlan plan_layer_bwd(int64_t S, int d_model, int Hq, int Hkv, int U) {
   return p;
 }
 
-GemmEpilogue heads_epi(bf16* n0, bf16* t0, bf16* n1, bf16* t1, int64_t n_split, int64_t Sp) {
+GemmEpilogue heads_epi(bf16* n0, bf16* n1, int64_t n_split, int64_t Sp) {
   GemmEpilogue e{};
   e.dst_norm[0] = n0;
-  e.dst_t[0] = t0;
   e.dst_norm[1] = n1;
-  e.dst_t[1] = t1;
   e.n_split = n_split;
   e.Sp = Sp;
   return e;
@@ -136,26 +134,25 @@ int run_layer_fwd(const bf16* x, const bf16* wqkv, const bf16* wo, bf16* y, bf16
   const LayerFwdPlan p = plan_layer_fwd(S, dm, Hq, Hkv, U);
   const int64_t Sp = p.Sp, ldw = (int64_t)(Hq + 2 * Hkv) * HEAD_DIM;
   bf16* Kp = (bf16*)(ws + p.Kp);
-  bf16* Vt = (bf16*)(ws + p.Vt);
+  bf16* Vp = (bf16*)(ws + p.Vp);
   bf16* Qc = (bf16*)(ws + p.Qc);
   bf16* Oc = (bf16*)(ws + p.Oc);
   float* Y32 = p.y32 ? (float*)(ws + p.Y32) : nullptr;
   const int G = Hq / Hkv;
   const GemmOperand X = operand(x, dm, S, dm);
-  // K | V = x [Wk | Wv]; K head-major for the score product, V transposed
-  // in MFMA order for the probability product.
+  // K | V = x [Wk | Wv], both head-major.
   UPIPE_LAUNCH(kGemm, st,
                gemm1(X, true, operand(wqkv + (int64_t)Hq * HEAD_DIM, ldw, 2 * Hkv * HEAD_DIM, dm),
-                     false, heads_epi(Kp, nullptr, nullptr, Vt, Hkv, Sp), GEMM_EPI_HEADS, Sp,
+                     false, heads_epi(Kp, Vp, Hkv, Sp), GEMM_EPI_HEADS, Sp,
                      2 * Hkv * HEAD_DIM, dm, st));
   const int nu = Hq / U;
   for (int c = 0; c < nu; ++c) {
     const int h0 = c * U;
     UPIPE_LAUNCH(kGemm, st,
                  gemm1(X, true, operand(wqkv + (int64_t)h0 * HEAD_DIM, ldw, U * HEAD_DIM, dm),
-                       false, heads_epi(Qc, nullptr, nullptr, nullptr, U, Sp), GEMM_EPI_HEADS, Sp,
+                       false, heads_epi(Qc, nullptr, U, Sp), GEMM_EPI_HEADS, Sp,
                        U * HEAD_DIM, dm, st));
-    UPIPE_LAUNCH(kAttnFwd, st, launch_attn_fwd(Qc, Kp, Vt, Oc, lse, S, Sp, U, h0, G, 1, st));
+    UPIPE_LAUNCH(kAttnFwd, st, launch_attn_fwd(Qc, Kp, Vp, Oc, lse, S, Sp, U, h0, G, 1, st));
     UPIPE_LAUNCH(kUnpackRows, st, launch_unpack_rows(Oc, S, Hq, h0, U, Sp, o_saved, st));
     // Y32 (+)= O_c Wo_c; O_c read head-major, Wo rows [h0*d, (h0+U)*d).
     UPIPE_LAUNCH(kGemm, st,
@@ -175,14 +172,11 @@ int run_layer_bwd(const bf16* x, const bf16* wqkv, const bf16* wo, const bf16* o
   char* ab = ws + p.attn_base;
   const int64_t Sp = p.Sp, ldw = (int64_t)(Hq + 2 * Hkv) * HEAD_DIM;
   bf16* Kp = (bf16*)(ab + a.Kp);
-  bf16* Kt = (bf16*)(ab + a.Kt);
   bf16* Vp = (bf16*)(ab + a.Vp);
   float* dK32 = a.carry ? (float*)(ab + a.dK32) : nullptr;
   float* dV32 = a.carry ? (float*)(ab + a.dV32) : nullptr;
   bf16* Qc = (bf16*)(ab + a.Qc);
-  bf16* Qct = (bf16*)(ab + a.Qct);
   bf16* dOc = (bf16*)(ab + a.dOc);
-  bf16* dOct = (bf16*)(ab + a.dOct);
   bf16* dQc = (bf16*)(ab + a.dQc);
   float* D = (float*)(ab + a.D);
   float* lse_c = (float*)(ab + a.lse_c);
@@ -212,10 +206,10 @@ int run_layer_bwd(const bf16* x, const bf16* wqkv, const bf16* wo, const bf16* o
     return UPIPE_OK;
   };
 
-  // Recompute K (head-major + transposed) and V (head-major).
+  // Recompute K and V (head-major).
   UPIPE_LAUNCH(kGemm, st,
                gemm1(X, true, operand(wqkv + (int64_t)Hq * HEAD_DIM, ldw, 2 * kvw, dm), false,
-                     heads_epi(Kp, Kt, Vp, nullptr, Hkv, Sp), GEMM_EPI_HEADS, Sp, 2 * kvw, dm,
+                     heads_epi(Kp, Vp, Hkv, Sp), GEMM_EPI_HEADS, Sp, 2 * kvw, dm,
                      st));
   const int nu = Hq / U;
   for (int c = 0; c < nu; ++c) {
@@ -224,7 +218,7 @@ int run_layer_bwd(const bf16* x, const bf16* wqkv, const bf16* wo, const bf16* o
     // dO_c = dY Wo_c^T (Wo rows of the chunk are k-contiguous).
     UPIPE_LAUNCH(kGemm, st,
                  gemm1(dY, true, operand(wo + (int64_t)h0 * HEAD_DIM * dm, dm, w, dm), true,
-                       heads_epi(dOc, dOct, nullptr, nullptr, U, Sp), GEMM_EPI_HEADS, Sp, w, dm,
+                       heads_epi(dOc, nullptr, U, Sp), GEMM_EPI_HEADS, Sp, w, dm,
                        st));
     UPIPE_LAUNCH(kRowdotLse, st,
                  launch_rowdot_lse(dOc, HEAD_DIM, Sp * HEAD_DIM, o_saved + (int64_t)h0 * HEAD_DIM,
@@ -234,16 +228,16 @@ int run_layer_bwd(const bf16* x, const bf16* wqkv, const bf16* wo, const bf16* o
     int rc = wgrad(operand(o_saved + (int64_t)h0 * HEAD_DIM, (int64_t)Hq * HEAD_DIM, w, S), dYn,
                    w, dm, dwo + (int64_t)h0 * HEAD_DIM * dm, dm, 0);
     if (rc != UPIPE_OK) return rc;
-    // Q_c recomputed, head-major + transposed.
+    // Q_c recomputed, head-major.
     UPIPE_LAUNCH(kGemm, st,
                  gemm1(X, true, operand(wqkv + (int64_t)h0 * HEAD_DIM, ldw, w, dm), false,
-                       heads_epi(Qc, Qct, nullptr, nullptr, U, Sp), GEMM_EPI_HEADS, Sp, w, dm,
+                       heads_epi(Qc, nullptr, U, Sp), GEMM_EPI_HEADS, Sp, w, dm,
                        st));
     UPIPE_LAUNCH(kAttnBwdDkdv, st,
-                 launch_attn_bwd_dkdv(Qc, Qct, dOc, dOct, lse_c, D, Kp, Vp, dK32, dV32, dKb, dVb,
-                                      S, Sp, U, h0, G, Hkv, 1, st));
+                 launch_attn_bwd_dkdv(Qc, dOc, lse_c, D, Kp, Vp, dK32, dV32, dKb, dVb, S, Sp, U,
+                                      h0, G, Hkv, 1, st));
     UPIPE_LAUNCH(kAttnBwdDq, st,
-                 launch_attn_bwd_dq(Qc, dOc, lse_c, D, Kp, Kt, Vp, dQc, S, Sp, U, h0, G, 1, st));
+                 launch_attn_bwd_dq(Qc, dOc, lse_c, D, Kp, Vp, dQc, S, Sp, U, h0, G, 1, st));
     // dX32 (+)= dQ_c Wq_c^T (Wqkv rows are k-contiguous in the chunk's columns).
     UPIPE_LAUNCH(kGemm, st,
                  gemm1(operand(dQc, HEAD_DIM, S, w, HEAD_DIM, Sp * HEAD_DIM), true,

@@ -5,7 +5,6 @@
 // and the stage output leaves through out_all_to_all into its slot of the
 // preallocated `final_out`.  On one GPU these become:
 //   pack   token-major [S, H, d] (chosen heads)  ->  head-major [n, Sp, d]
-//          (+ optionally the transposed copy [n, d, Sp] in MFMA order)
 //   unpack head-major [n, Sp, d]                 ->  token-major [S, H, d]
 // Rows S..Sp-1 of packed buffers are zero, so the attention kernels never
 // test sequence bounds on loads.  All kernels are HBM-bound copies.
@@ -14,12 +13,10 @@
 
 namespace upipe {
 
-// One workgroup packs a 64-row slab of one head.  256 threads, each moving
-// four 16-byte pieces; the transposed copy goes through LDS.
+// One workgroup packs a 64-row slab of one head; 256 threads, each moving
+// four 16-byte pieces.
 __global__ __launch_bounds__(256) void pack_rows_kernel(
-    const bf16* __restrict__ src, int64_t S, int H, int h0, int64_t Sp,
-    bf16* __restrict__ dst, bf16* __restrict__ dst_t) {
-  __shared__ __attribute__((aligned(16))) bf16 tile[64][HEAD_DIM + 8];
+    const bf16* __restrict__ src, int64_t S, int H, int h0, int64_t Sp, bf16* __restrict__ dst) {
   const int t = threadIdx.x;
   const int hh = blockIdx.y;
   const int64_t s0 = (int64_t)blockIdx.x * 64;
@@ -32,20 +29,7 @@ __global__ __launch_bounds__(256) void pack_rows_kernel(
     u32x4 val = {0u, 0u, 0u, 0u};
     if (s < S)
       val = *reinterpret_cast<const u32x4*>(src + (s * H + h) * HEAD_DIM + chunk * 8);
-    if (dst)
-      *reinterpret_cast<u32x4*>(dst + ((int64_t)hh * Sp + s) * HEAD_DIM + chunk * 8) = val;
-    if (dst_t) *reinterpret_cast<u32x4*>(&tile[row][chunk * 8]) = val;
-  }
-  if (!dst_t) return;
-  __syncthreads();
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int pi = t + 256 * r;
-    const int drow = pi >> 3, c = pi & 7;
-    bf16x8 out;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) out[j] = tile[perm16(8 * c + j)][drow];
-    *reinterpret_cast<bf16x8*>(dst_t + ((int64_t)hh * HEAD_DIM + drow) * Sp + s0 + 8 * c) = out;
+    *reinterpret_cast<u32x4*>(dst + ((int64_t)hh * Sp + s) * HEAD_DIM + chunk * 8) = val;
   }
 }
 
@@ -97,10 +81,9 @@ __global__ __launch_bounds__(256) void rowdot_lse_kernel(
 }
 
 hipError_t launch_pack_rows(const bf16* src, int64_t S, int H, int h0, int n,
-                            int64_t Sp, bf16* dst, bf16* dst_t, hipStream_t st) {
+                            int64_t Sp, bf16* dst, hipStream_t st) {
   dim3 grid((unsigned)(Sp / 64), (unsigned)n);
-  hipLaunchKernelGGL(pack_rows_kernel, grid, dim3(256), 0, st, src, S, H, h0,
-                     Sp, dst, dst_t);
+  hipLaunchKernelGGL(pack_rows_kernel, grid, dim3(256), 0, st, src, S, H, h0, Sp, dst);
   return hipGetLastError();
 }
 
