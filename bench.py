@@ -110,12 +110,16 @@ def cpu_baseline(w, q, k, v, do, target_s):
         A.attn_bwd(*args)
         return time.perf_counter() - t0
 
+    # Time grows ~ S'^2 once the fixed overheads are amortised: grow S' from
+    # a small probe until one run takes at least 0.6 x target_s.
     sp = 2048
     t = run(sp)
-    # time grows ~ S'^2; aim for target_s
-    scale = (target_s / max(t, 1e-3)) ** 0.5
-    sp = int(min(w.S, max(2048, (sp * scale) // 128 * 128)))
-    t = run(sp)
+    for _ in range(4):
+        if t >= 0.6 * target_s or sp >= w.S:
+            break
+        scale = (target_s / max(t, 1e-3)) ** 0.5
+        sp = int(min(w.S, max(sp + 128, (sp * scale) // 128 * 128)))
+        t = run(sp)
     pairs = sp * (sp + 1) // 2
     flops = 3.5 * 4 * w.d * pairs
     return {"value": round(flops / t / 1e12, 6), "unit": "TFLOP/s",

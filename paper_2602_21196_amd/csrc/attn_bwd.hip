@@ -11,9 +11,9 @@
 //         K and V fragments in registers) and walks the chunk's query heads in
 //         ascending order and, within a head, the 128-row query tiles from the
 //         last one down to its diagonal (each tile as 64-row halves, upper
-//         first, and each half as two 32-row subtiles in ascending order), so
-//         that all resident workgroups read the same query tiles at about the
-//         same time (shared L2 lines).  Its
+//         first, and each half as two 32-row subtiles, upper first), so that
+//         all resident workgroups read the same query tiles at about the same
+//         time (shared L2 lines).  Its
 //         fp32 dK/dV accumulators start from the values the previous chunk
 //         left in the workspace (UPipe keeps per-group dK/dV accumulators alive
 //         across stages, Appendix A), so any chunk size U gives bit-identical
@@ -92,13 +92,9 @@ __device__ __forceinline__ void read_dvdk(const char* buf, int sub, int lane, Fr
     }
 }
 
-// Scores of one subtile from its fragments, then P and dS (bf16 A operands).
-template <bool CAUSAL>
-__device__ __forceinline__ void subtile_pds(const Frags& fr, const char* buf, int sub, uint32_t qs,
-                                            uint32_t mykey, bool diag, int g,
-                                            const bf16x8 (&kf)[8], const bf16x8 (&vf)[8],
-                                            bf16x8 (&pf)[2], bf16x8 (&sf)[2]) {
-  f32x16 sacc, pacc;
+// S^T and dP^T of one subtile from its fragments (16 MFMAs).
+__device__ __forceinline__ void subtile_sdp(const Frags& fr, const bf16x8 (&kf)[8],
+                                            const bf16x8 (&vf)[8], f32x16& sacc, f32x16& pacc) {
 #pragma unroll
   for (int i = 0; i < 16; ++i) { sacc[i] = 0.f; pacc[i] = 0.f; }
 #pragma unroll
@@ -106,6 +102,14 @@ __device__ __forceinline__ void subtile_pds(const Frags& fr, const char* buf, in
     sacc = mfma32x32x16(fr.f[2 * s], kf[s], sacc);
     pacc = mfma32x32x16(fr.f[2 * s + 1], vf[s], pacc);
   }
+}
+
+// P and dS of one subtile (rows `sub`.. of the tile, first row qs) as bf16 A
+// operands, from its scores and the staged lse / D rows.
+template <bool CAUSAL>
+__device__ __forceinline__ void subtile_pds(const f32x16& sacc, const f32x16& pacc, const char* buf,
+                                            int sub, uint32_t qs, uint32_t mykey, bool diag, int g,
+                                            bf16x8 (&pf)[2], bf16x8 (&sf)[2]) {
   const float* lsel = reinterpret_cast<const float*>(buf + OFF_LSE) + sub;
   const float* Dl = reinterpret_cast<const float*>(buf + OFF_D) + sub;
   float p[16];
@@ -144,30 +148,55 @@ __device__ __forceinline__ void dvdk_products(const Frags& fr, const bf16x8 (&pf
     }
 }
 
-// One pair of subtiles (rows base..base+63 of the tile).  The first subtile
-// of the pair is computed even where only the second is needed: the diagonal
-// mask then zeroes all of its P and dS.  Each block of 16 MFMAs finds its LDS
-// fragments already read: the reads of the next block are issued before the
-// products of the current one.
+// Scheduling request for a region of 16 MFMAs and the VALU work of one
+// subtile's P and dS: its LDS reads first, then one MFMA after every few VALU
+// instructions, so the matrix unit and the vector ALU of the one wave on the
+// SIMD work side by side.
+constexpr int KV_NV = 5;   // VALU instructions requested between two MFMAs
+__device__ __forceinline__ void interleave_mfma_valu() {
+  __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x002, KV_NV, 0);
+  }
+}
+
+// One pair of subtiles (rows base..base+63 of the tile), in four fenced
+// regions so that each block of 16 MFMAs shares its region with VALU work it
+// does not depend on:
+//   A: S/dP products of the upper subtile
+//   B: S/dP products of the lower subtile   | P, dS of the upper subtile
+//   C: dV/dK products of the upper subtile  | P, dS of the lower subtile
+//   D: dV/dK products of the lower subtile
+// The LDS fragments of each block are read one region ahead.  The lower
+// subtile is computed even where only the upper one is needed: the diagonal
+// mask then zeroes all of its P and dS.
 template <bool CAUSAL>
 __device__ __forceinline__ void pair_step(const char* buf, int base, uint32_t qb, uint32_t kw,
                                           uint32_t mykey, int r32, int g, int lane,
                                           const bf16x8 (&kf)[8], const bf16x8 (&vf)[8],
                                           f32x16 (&dva)[4], f32x16 (&dka)[4]) {
   Frags fa, fb;
+  f32x16 s1, p1, s0, p0;
   bf16x8 pf1[2], sf1[2], pf0[2], sf0[2];
   const uint32_t q1 = qb + base + 32, q0 = qb + base;
   read_sdp(buf, base + 32, r32, g, fa);
   read_sdp(buf, base, r32, g, fb);
   __builtin_amdgcn_sched_barrier(0);
-  subtile_pds<CAUSAL>(fa, buf, base + 32, q1, mykey, q1 < kw + 31, g, kf, vf, pf1, sf1);
-  read_dvdk(buf, base, lane, fa);
+  subtile_sdp(fa, kf, vf, s1, p1);                                            // A
+  read_dvdk(buf, base + 32, lane, fa);
   __builtin_amdgcn_sched_barrier(0);
-  subtile_pds<CAUSAL>(fb, buf, base, q0, mykey, q0 < kw + 31, g, kf, vf, pf0, sf0);
-  read_dvdk(buf, base + 32, lane, fb);
+  subtile_sdp(fb, kf, vf, s0, p0);                                            // B
+  subtile_pds<CAUSAL>(s1, p1, buf, base + 32, q1, mykey, q1 < kw + 31, g, pf1, sf1);
+  read_dvdk(buf, base, lane, fb);
+  interleave_mfma_valu();
   __builtin_amdgcn_sched_barrier(0);
-  dvdk_products(fa, pf0, sf0, dva, dka);
-  dvdk_products(fb, pf1, sf1, dva, dka);
+  dvdk_products(fa, pf1, sf1, dva, dka);                                      // C
+  subtile_pds<CAUSAL>(s0, p0, buf, base, q0, mykey, q0 < kw + 31, g, pf0, sf0);
+  interleave_mfma_valu();
+  __builtin_amdgcn_sched_barrier(0);
+  dvdk_products(fb, pf0, sf0, dva, dka);                                      // D
 }
 
 template <bool CAUSAL>
