@@ -122,10 +122,37 @@ def cpu_baseline(w, q, k, v, do, target_s):
         t = run(sp)
     pairs = sp * (sp + 1) // 2
     flops = 3.5 * 4 * w.d * pairs
+    full_pairs = w.S * (w.S + 1) // 2 * w.Hq
     return {"value": round(flops / t / 1e12, 6), "unit": "TFLOP/s",
             "cores": cores, "kind": "oracle",
             "sample": f"causal prefix S'={sp} of {w.name}, 1 query head "
-                      f"(kv head 0), fwd+bwd, float64 numpy, {t:.1f} s"}
+                      f"(kv head 0), fwd+bwd, float64 numpy, {t:.1f} s",
+            "extrapolated_full_s": round(t * full_pairs / pairs, 1),
+            "extrapolated_note": "whole workload (all heads, full S) at the "
+                                 "sampled rate; extrapolated, not run"}
+
+
+def workspace_model_gb(S, Hq, Hkv, d, U):
+    """Attention-only backward workspace model A + B U (the larger of the two
+    workspaces): resident packed K, V (+ fp32 dK, dV carries when a key/value
+    group spans chunks) and, per chunk head, Q, dO, dQ (bf16) and lse, D."""
+    Sp = (S + 127) // 128 * 128
+    G = Hq // Hkv   # a group spans chunks when its first and last heads differ in h // U
+    carry = any((g * G) // U != ((g + 1) * G - 1) // U for g in range(Hkv))
+    fixed = 2 * Sp * Hkv * d * 2 + (2 * Sp * Hkv * d * 4 if carry else 0)
+    return (fixed + U * Sp * (3 * d * 2 + 2 * 4)) / 1e9
+
+
+def linear_fit(xs, ys):
+    """Least-squares y = A + B x and R^2."""
+    n = len(xs)
+    mx, my = sum(xs) / n, sum(ys) / n
+    sxx = sum((x - mx) ** 2 for x in xs)
+    B = sum((x - mx) * (y - my) for x, y in zip(xs, ys)) / sxx if sxx else 0.0
+    A = my - B * mx
+    ss_tot = sum((y - my) ** 2 for y in ys)
+    ss_res = sum((y - (A + B * x)) ** 2 for x, y in zip(xs, ys))
+    return A, B, (1.0 - ss_res / ss_tot) if ss_tot else 1.0
 
 
 def main():
@@ -239,9 +266,17 @@ def main():
             sweep_tf[str(u)] = round(step_flops / ((time.perf_counter() - t1) / 2) / 1e12, 2)
             del o, lse, g
         out["peak_activation_gb_vs_U"] = sweep_mem
+        out["peak_activation_model_gb_vs_U"] = {
+            str(u): round(workspace_model_gb(S, Hq, Hkv, d, u), 4) for u in w.U_sweep}
+        us = [int(u) for u in sweep_mem]
+        A, B, r2 = linear_fit(us, [sweep_mem[str(u)] for u in us])
+        out["peak_activation_fit"] = {"A_gb": round(A, 4), "B_gb_per_U": round(B, 4),
+                                      "r2": round(r2, 4)}
         out["peak_activation_note"] = (
             "max_memory_allocated during one fwd+bwd above the resident "
-            "inputs, minus the outputs o, lse, dq, dk, dv: the workspaces")
+            "inputs, minus the outputs o, lse, dq, dk, dv: the workspaces; "
+            "the model drops the fp32 dK/dV carries once U is a multiple of "
+            "the group size, so the fit over all U is not exactly linear")
         out["tflops_vs_U"] = sweep_tf
 
     if not args.no_cpu_baseline and not w.is_layer:
