@@ -56,7 +56,9 @@ struct GemmEpilogue {
 };
 
 // M and N must be multiples of 128.  The k range [k_begin, k_begin + k_total)
-// is cut into `splits` pieces of k_len (a multiple of 32).  Supported
+// is cut into `splits` pieces of k_len; k_begin and k_len are multiples of
+// 128, and so is k_total when an operand is K-major (hipErrorInvalidValue
+// otherwise).  Supported
 // combinations: (A K-major, B MN-major, HEADS | ACC32), (A K-major, B K-major,
 // HEADS | ACC32), (A MN-major, B MN-major, PARTIAL).
 hipError_t launch_gemm(const GemmOperand& A, bool a_kmajor, const GemmOperand& B, bool b_kmajor,

@@ -3,19 +3,24 @@
 //
 // The block needs nine differently laid-out products (QKV projection slice,
 // output projection, their data and weight gradients; paper Section 3.3 and
-// Appendix A).  Instead of transposing tensors in HBM, each operand is
-// described by a small descriptor and staged into LDS as [row][k] tiles:
-//   K-major operand   (k contiguous in memory)  : 16-byte rows copied as is;
-//   MN-major operand  (m or n contiguous)       : 8x8 bf16 blocks loaded as
-//     eight 16-byte rows and transposed in registers (v_perm_b32) on the way.
+// Appendix A).  No tensor is transposed in HBM.  Every operand tile is staged
+// into LDS exactly as it lies in memory -- 128 rows of 256 bytes:
+//   K-major operand  (k contiguous)    : rows = m (or n), 128 k per row;
+//   MN-major operand (m/n contiguous)  : rows = k, 128 m (or n) per row --
+// by buffer->LDS copies (no register staging), and the MFMA fragments are
+// read in one common k order:
+//   two K-major operands       : plain 16-byte reads (k = 8g + 0..7);
+//   an MN-major operand        : transposing reads (tr_operand, k = 4g + 0..3,
+//                                8 + 4g + 0..3), and a K-major partner then
+//                                reads the same k as two 8-byte halves.
 // Operands may be split into 128-wide blocks with their own stride (the
 // head-major chunk buffers [U][Sp][128]).
 //
-// Tile: 128 x 128 per workgroup, 4 waves as 2 x 2 of 64 x 64, BK = 32,
-// double-buffered LDS.  The k loop runs in ascending order with one fp32
-// accumulator chain per output element, so a product split over several
-// calls (k ranges accumulated through an fp32 buffer) is bitwise equal to a
-// single call over the whole k range.
+// Tile: 128 x 128 per workgroup, 4 waves as 2 x 2 of 64 x 64, BK = 128,
+// double-buffered (128 KB of LDS) except for the fp32-accumulating products.  The k loop runs in ascending order with
+// one fp32 accumulator chain per output element, so a product split over
+// several calls (k ranges accumulated through an fp32 buffer) is bitwise equal
+// to a single call over the whole k range.
 #include "common.h"
 #include "gemm.h"
 
@@ -23,100 +28,83 @@ namespace upipe {
 
 namespace {
 
-constexpr int BM = 128, BN = 128, BKG = 32;
-constexpr int TILE_BYTES = BM * BKG * 2;  // 8 KB per operand per stage
+constexpr int BM = 128, BN = 128, BKG = 128;
+constexpr int TILE_BYTES = 128 * 256;     // 32 KB per operand per stage
 
-__device__ __forceinline__ uint32_t t_off(int row, int chunk) {
-  return row * 64 + ((chunk ^ ((row >> 1) & 3)) << 4);
-}
-
-__device__ __forceinline__ const bf16* kmajor_ptr(const GemmOperand& o, int64_t r, int64_t k) {
-  return o.p + (k / o.blk) * o.blk_stride + r * o.ld + (k % o.blk);
-}
-__device__ __forceinline__ const bf16* mnmajor_ptr(const GemmOperand& o, int64_t r, int64_t k) {
+// Address of operand element (r, k).
+__device__ __forceinline__ const bf16* elem_ptr(const GemmOperand& o, bool kmajor, int64_t r,
+                                                int64_t k) {
+  if (kmajor) return o.p + (k / o.blk) * o.blk_stride + r * o.ld + (k % o.blk);
   return o.p + (r / o.blk) * o.blk_stride + k * o.ld + (r % o.blk);
 }
 
-struct OpRegs {
-  u32x4 v[8];
-};
-
-// K-major: 512 pieces (128 rows x 4 chunks) per tile, two per thread.
-__device__ __forceinline__ void load_kmajor(OpRegs& r, const GemmOperand& o, int64_t r0,
-                                            int64_t k0, int t) {
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int pi = t + 256 * i;
-    const int row = pi >> 2, c = pi & 3;
-    const int64_t gr = r0 + row, gk = k0 + 8 * c;
-    u32x4 val = {0u, 0u, 0u, 0u};
-    if (gr < o.rows_valid && gk < o.k_valid)
-      val = *reinterpret_cast<const u32x4*>(kmajor_ptr(o, gr, gk));
-    r.v[i] = val;
-  }
-}
-__device__ __forceinline__ void store_kmajor(const OpRegs& r, char* buf, int t) {
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int pi = t + 256 * i;
-    lds_write_b128(buf, t_off(pi >> 2, pi & 3), r.v[i]);
-  }
+// Buffer resource over the operand's tile at (r0, k0), bounded by the valid
+// rows (K-major: rows r0.. < rows_valid) or valid k (MN-major: k0.. <
+// k_valid), so that padding reads as zero.
+__device__ __forceinline__ buf_rsrc tile_rsrc(const GemmOperand& o, bool kmajor, int64_t r0,
+                                              int64_t k0) {
+  const int64_t n_lines = kmajor ? o.rows_valid - r0 : o.k_valid - k0;   // 256-B lines in use
+  int64_t bytes = n_lines <= 0 ? 0 : ((n_lines > 128 ? 127 : n_lines - 1) * o.ld + 128) * 2;
+  return make_rsrc(elem_ptr(o, kmajor, r0, k0), (uint32_t)bytes);
 }
 
-// MN-major: 64 blocks of 8 (k) x 8 (rows) per tile; threads [base, base+64).
-__device__ __forceinline__ void load_mnmajor(OpRegs& r, const GemmOperand& o, int64_t r0,
-                                             int64_t k0, int tl) {
-  const int kb = tl >> 4, rb = tl & 15;
+// This wave's share of one operand tile: 8 blocks of 4 lines of 256 B.  The
+// lane offsets `off` place line chunk c at LDS chunk c ^ tsw(line).
+__device__ __forceinline__ void issue_tile(buf_rsrc r, const uint32_t (&off)[8], char* tile, int w) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) dma_buf_b128(r, off[i], 0, tile + (8 * w + i) * 1024);
+}
+
+__device__ __forceinline__ void lane_offsets(int64_t ld, int w, int lane, uint32_t (&off)[8]) {
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    const int64_t gk = k0 + 8 * kb + i, gr = r0 + 8 * rb;
-    u32x4 val = {0u, 0u, 0u, 0u};
-    if (gk < o.k_valid && gr < o.rows_valid)
-      val = *reinterpret_cast<const u32x4*>(mnmajor_ptr(o, gr, gk));
-    r.v[i] = val;
-  }
-}
-// In: v[i] = row-block (8 rows) at k = 8kb+i.  Out: LDS row 8rb+m gets the
-// 8 k-values of that row as one 16-byte chunk.
-__device__ __forceinline__ void store_mnmajor(const OpRegs& r, char* buf, int tl) {
-  const int kb = tl >> 4, rb = tl & 15;
-#pragma unroll
-  for (int m = 0; m < 8; ++m) {
-    const int p = m >> 1;
-    const uint32_t sel = (m & 1) ? 0x07060302u : 0x05040100u;
-    u32x4 out;
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      out[j] = __builtin_amdgcn_perm(r.v[2 * j + 1][p], r.v[2 * j][p], sel);
-    lds_write_b128(buf, t_off(8 * rb + m, kb), out);
+    const int line = 4 * (8 * w + i) + (lane >> 4);
+    off[i] = (uint32_t)(line * ld * 2) + (((lane & 15) ^ tsw(line)) << 4);
   }
 }
 
-template <bool A_K, bool B_K>
-struct Loader {
-  OpRegs a, b;
-  __device__ __forceinline__ void load(const GemmOperand& A, const GemmOperand& B, int64_t m0,
-                                       int64_t n0, int64_t k0, int t) {
-    if (A_K) load_kmajor(a, A, m0, k0, t);
-    else if (t < 64) load_mnmajor(a, A, m0, k0, t);
-    if (B_K) load_kmajor(b, B, n0, k0, t);
-    else if (t >= 64 && t < 128) load_mnmajor(b, B, n0, k0, t - 64);
+// Fragment of the 32 rows (m or n) r0.. at k-step ks (16 k) of one tile.
+//   KM_PLAIN: K-major tile, k = 16 ks + 8g + 0..7
+//   KM_TR   : K-major tile, k = 16 ks + 4g + 0..3, 16 ks + 8 + 4g + 0..3
+//   MN      : MN-major tile (transposing reads), same k order as KM_TR
+enum { KM_PLAIN = 0, KM_TR = 1, MN_TR = 2 };
+template <int MODE>
+__device__ __forceinline__ bf16x8 frag(const char* tile, int r0, int ks, int lane) {
+  const int r32 = lane & 31, g = lane >> 5;
+  if (MODE == KM_PLAIN) return lds_read_b128(tile, swzt(r0 + r32, 2 * ks + g));
+  if (MODE == MN_TR) return tr_operand(tile, 16 * ks, r0, lane);
+  typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+  const bf16x4 lo = *(const lds_bf16x4*)(tile + swzt(r0 + r32, 2 * ks) + 8 * g);
+  const bf16x4 up = *(const lds_bf16x4*)(tile + swzt(r0 + r32, 2 * ks + 1) + 8 * g);
+  bf16x8 v;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    v[e] = lo[e];
+    v[4 + e] = up[e];
   }
-  __device__ __forceinline__ void store(char* bufA, char* bufB, int t) {
-    if (A_K) store_kmajor(a, bufA, t);
-    else if (t < 64) store_mnmajor(a, bufA, t);
-    if (B_K) store_kmajor(b, bufB, t);
-    else if (t >= 64 && t < 128) store_mnmajor(b, bufB, t - 64);
-  }
+  return v;
+}
+
+// The fp32-accumulating products have short k ranges (one head chunk) and
+// are bound by the read-modify-write of the fp32 buffer: one stage of LDS
+// (64 KB) lets two workgroups share a CU.  The others stream long k ranges and
+// double-buffer (128 KB, one workgroup per CU).
+template <int EPI>
+struct GemmStages {
+  static constexpr int N = EPI == GEMM_EPI_ACC32 ? 1 : 2;
 };
 
 template <bool A_K, bool B_K, int EPI>
-__global__ __launch_bounds__(256, 2) void gemm_kernel(GemmOperand A, GemmOperand B, GemmEpilogue E,
-                                                      int64_t M, int64_t N, int64_t k_begin,
-                                                      int64_t k_len) {
-  __shared__ __attribute__((aligned(16))) char smem[4 * TILE_BYTES];
+__global__ __launch_bounds__(256, 3 - GemmStages<EPI>::N) void gemm_kernel(
+    GemmOperand A, GemmOperand B, GemmEpilogue E, int64_t M, int64_t N, int64_t k_begin,
+    int64_t k_len) {
+  constexpr int AM = A_K ? (B_K ? KM_PLAIN : KM_TR) : MN_TR;
+  constexpr int BMODE = B_K ? (A_K ? KM_PLAIN : KM_TR) : MN_TR;
+  constexpr int NST = GemmStages<EPI>::N;
+  __shared__ __attribute__((aligned(1024))) char smem[NST * 2 * TILE_BYTES];
   const int t = threadIdx.x;
-  const int lane = t & 63, w = t >> 6;
+  const int lane = t & 63;
+  const int w = __builtin_amdgcn_readfirstlane(t >> 6);
   const int r32 = lane & 31, g = lane >> 5;
   const int wm = w >> 1, wn = w & 1;
   const int64_t tiles_n = N / BN;
@@ -126,7 +114,7 @@ __global__ __launch_bounds__(256, 2) void gemm_kernel(GemmOperand A, GemmOperand
   const int64_t kb0 = k_begin + split * k_len;
   int64_t kend = kb0 + k_len;
   if (kend > k_begin + E.k_total) kend = k_begin + E.k_total;
-  const int nk = (int)((kend - kb0 + BKG - 1) / BKG);
+  const int nk = kend > kb0 ? (int)((kend - kb0 + BKG - 1) / BKG) : 0;
 
   f32x16 acc[2][2];
   if (EPI == GEMM_EPI_ACC32 && !E.first) {
@@ -150,36 +138,38 @@ __global__ __launch_bounds__(256, 2) void gemm_kernel(GemmOperand A, GemmOperand
         for (int i = 0; i < 16; ++i) acc[mt][nt][i] = 0.f;
   }
 
-  Loader<A_K, B_K> ld;
-  if (nk > 0) {
-    ld.load(A, B, m0, n0, kb0, t);
-    ld.store(smem, smem + TILE_BYTES, t);
-  }
-  __syncthreads();
+  uint32_t offa[8], offb[8];
+  lane_offsets(A.ld, w, lane, offa);
+  lane_offsets(B.ld, w, lane, offb);
+  auto issue = [&](int kk) {
+    const int64_t k0 = kb0 + (int64_t)kk * BKG;
+    char* buf = smem + (kk % NST) * 2 * TILE_BYTES;
+    issue_tile(tile_rsrc(A, A_K, m0, k0), offa, buf, w);
+    issue_tile(tile_rsrc(B, B_K, n0, k0), offb, buf + TILE_BYTES, w);
+  };
+  if (nk > 0) issue(0);
   for (int kk = 0; kk < nk; ++kk) {
-    char* bufA = smem + (kk & 1) * 2 * TILE_BYTES;
-    char* bufB = bufA + TILE_BYTES;
-    const bool more = kk + 1 < nk;
-    if (more) ld.load(A, B, m0, n0, kb0 + (int64_t)(kk + 1) * BKG, t);
+    const char* bufA = smem + (kk % NST) * 2 * TILE_BYTES;
+    const char* bufB = bufA + TILE_BYTES;
+    if (NST == 1 && kk > 0) {
+      __syncthreads();   // every wave is done with stage kk-1
+      issue(kk);
+    }
+    wait_vmem();
+    __syncthreads();   // stage kk landed for all waves; stage kk-1's buffer is free
+    if (NST == 2 && kk + 1 < nk) issue(kk + 1);
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
+    for (int ks = 0; ks < BKG / 16; ++ks) {
       bf16x8 af[2], bfr[2];
 #pragma unroll
-      for (int mt = 0; mt < 2; ++mt)
-        af[mt] = lds_read_b128(bufA, t_off(64 * wm + 32 * mt + r32, 2 * ks + g));
+      for (int mt = 0; mt < 2; ++mt) af[mt] = frag<AM>(bufA, 64 * wm + 32 * mt, ks, lane);
 #pragma unroll
-      for (int nt = 0; nt < 2; ++nt)
-        bfr[nt] = lds_read_b128(bufB, t_off(64 * wn + 32 * nt + r32, 2 * ks + g));
+      for (int nt = 0; nt < 2; ++nt) bfr[nt] = frag<BMODE>(bufB, 64 * wn + 32 * nt, ks, lane);
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
         for (int nt = 0; nt < 2; ++nt) acc[mt][nt] = mfma32x32x16(af[mt], bfr[nt], acc[mt][nt]);
     }
-    if (more) {
-      char* nA = smem + ((kk + 1) & 1) * 2 * TILE_BYTES;
-      ld.store(nA, nA + TILE_BYTES, t);
-    }
-    __syncthreads();
   }
 
   // ---- epilogues.  Lane holds column n = n0 + 64wn + 32nt + r32 and rows
@@ -248,6 +238,11 @@ hipError_t launch_t(const GemmOperand& A, const GemmOperand& B, const GemmEpilog
 hipError_t launch_gemm(const GemmOperand& A, bool a_kmajor, const GemmOperand& B, bool b_kmajor,
                        const GemmEpilogue& E, int epi, int64_t M, int64_t N, int64_t k_begin,
                        int64_t k_len, int splits, hipStream_t st) {
+  // A K-major tile reads 128 consecutive k of each row: the k range must be
+  // made of whole tiles (an MN-major operand is bounded by its buffer
+  // resource instead); pieces must start on tile boundaries.
+  if ((M % BM) || (N % BN) || (k_len % BKG) || (k_begin % BKG)) return hipErrorInvalidValue;
+  if ((a_kmajor || b_kmajor) && (E.k_total % BKG)) return hipErrorInvalidValue;
 #define UPIPE_GEMM_CASE(AK, BK_, EP)                                               \
   if (a_kmajor == AK && b_kmajor == BK_ && epi == EP)                              \
     return launch_t<AK, BK_, EP>(A, B, E, M, N, k_begin, k_len, splits, st);

@@ -123,7 +123,7 @@ GemmEpilogue acc_epi(float* c32, int64_t ldc, bf16* out, int64_t ldo, int64_t m_
 hipError_t gemm1(const GemmOperand& A, bool ak, const GemmOperand& B, bool bk, GemmEpilogue E,
                  int epi, int64_t M, int64_t N, int64_t K, hipStream_t st) {
   E.k_total = K;
-  return launch_gemm(A, ak, B, bk, E, epi, M, N, 0, round_up(K, 32), 1, st);
+  return launch_gemm(A, ak, B, bk, E, epi, M, N, 0, round_up(K, 128), 1, st);
 }
 
 }  // namespace
