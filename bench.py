@@ -166,6 +166,8 @@ def main():
     from paper_2602_21196_amd import upipe
 
     w = W.WORKLOADS[args.workload]
+    if w.extra.get("ring"):
+        return ring_bench(args, w)
     dev = "cuda:0"
     S, Hq, Hkv, d, U = w.S, w.Hq, w.Hkv, w.d, args.U
     fwd_flops, bwd_flops = W.attention_flops(S, Hq, d)
@@ -281,6 +283,115 @@ def main():
 
     if not args.no_cpu_baseline and not w.is_layer:
         out["cpu_baseline"] = cpu_baseline(w, q, k, v, do, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+def ring_cpu_baseline(w, q, k, v, delta, target_s):
+    """Oracle ring step (float64 numpy) on a bounded block: the first n query
+    rows against the first n keys at the workload's offsets, one query head."""
+    import numpy as np
+    from oracle import ring as R
+    import workloads as W
+
+    def run(n):
+        f = lambda t, m: t[:m, :1].float().double().numpy()  # noqa: E731
+        args = (f(q, n), f(k, n), f(v, n))
+        t0 = time.perf_counter()
+        R.attn_fwd_offset(*args, delta, True)
+        return time.perf_counter() - t0
+
+    n = 1024
+    t = run(n)
+    for _ in range(4):
+        if t >= 0.6 * target_s or n >= min(w.S, w.extra["kv_len"]):
+            break
+        n = int(min(w.S, w.extra["kv_len"], max(n + 128, n * (target_s / max(t, 1e-3)) ** 0.5)))
+        t = run(n)
+    pairs = W.ring_pairs(n, n, delta)
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        cores = os.cpu_count()
+    return {"value": round(4 * w.d * pairs / t / 1e12, 6), "unit": "TFLOP/s", "cores": cores,
+            "kind": "oracle",
+            "sample": f"first {n} query rows x first {n} keys of {w.name}, 1 query head, "
+                      f"ring-step forward, float64 numpy, {t:.1f} s"}
+
+
+def ring_bench(args, w):
+    """One ring step (query block against one key/value block at its offset)
+    plus the merge of its partial result into the running one."""
+    import torch
+    import workloads as W
+    from paper_2602_21196_amd import upipe
+    dev = "cuda:0"
+    Sq, Skv, Hq, Hkv, d, U = w.S, w.extra["kv_len"], w.Hq, w.Hkv, w.d, args.U
+    qo, ko = w.extra["q_offset"], w.extra["kv_offset"]
+    q, k, v = W.inputs_for(w)
+    qd, kd, vd = (t.to(dev) for t in (q, k, v))
+    ws = upipe.workspace(upipe.upipe_attn_fwd_ring_workspace_size(Sq, Skv, Hq, Hkv, d, U), dev)
+    # the running result before this step: the query block's own causal block
+    o_acc, lse_acc = upipe.attn_fwd_ring(qd, qd[:, :Hkv].contiguous(), qd[:, :Hkv].contiguous(),
+                                         qo, qo, causal=True, U=U)
+    flops = 4 * d * Hq * W.ring_pairs(Sq, Skv, qo - ko)
+
+    def step():
+        o_p, lse_p = upipe.attn_fwd_ring(qd, kd, vd, qo, ko, causal=True, U=U, ws=ws)
+        upipe.lse_merge(o_acc, lse_acc, o_p, lse_p)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    upipe.upipe_profile_reset()
+    upipe.upipe_profile_enable(1)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    upipe.upipe_profile_enable(0)
+    kernels = {}
+    for name in upipe.upipe_profile_names():
+        n, ms = upipe.upipe_profile_query(name)
+        if n:
+            kernels[name] = {"launches_per_step": n // args.steps,
+                             "ms_per_step": round(ms / args.steps, 4),
+                             "avg_launch_ms": round(ms / n, 4)}
+    upipe.upipe_profile_reset()
+    fw = kernels.get("attn_fwd", {})
+    fwd_tf = flops / (fw["ms_per_step"] * 1e-3) / 1e12 if fw else None
+    if fw:
+        fw["tflops"] = round(fwd_tf, 2)
+    mg = kernels.get("lse_merge")
+    merge_bytes = 3 * Sq * Hq * d * 2 + 3 * Hq * Sq * 4    # o, o_p read, o written; lse likewise
+    if mg:
+        mg["gb_per_s"] = round(merge_bytes / (mg["avg_launch_ms"] * 1e-3) / 1e9, 1)
+    value = flops / (elapsed / args.steps) / 1e12
+    out = {"metric": "ring step: attention forward over one key/value block + LSE merge, "
+                     "TFLOP/s per MI355X",
+           "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": round(elapsed / args.steps * 1e3, 3),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+           "data": "synthetic",
+           "config": {"workload": w.name, "Sq": Sq, "Skv": Skv, "q_offset": qo,
+                      "kv_offset": ko, "Hq": Hq, "Hkv": Hkv, "d": d, "U": U, "causal": True,
+                      "seed": w.seed},
+           "frac_of_peak": round(value / PEAK_BF16_TFLOPS, 4),
+           "roofline": {"kernel": "attn_fwd", "bound": "mfma",
+                        "achieved": round(fwd_tf, 2) if fwd_tf else None,
+                        "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                        "frac": round(fwd_tf / PEAK_BF16_TFLOPS, 4) if fwd_tf else None,
+                        "traffic": None, "traffic_unit": "bytes per launch"},
+           "merge_roofline": {"kernel": "lse_merge", "bound": "hbm",
+                              "achieved": mg["gb_per_s"] if mg else None, "peak": PEAK_HBM_GBS,
+                              "unit": "GB/s",
+                              "frac": round(mg["gb_per_s"] / PEAK_HBM_GBS, 4) if mg else None,
+                              "bytes_per_launch": merge_bytes},
+           "kernels": kernels}
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = ring_cpu_baseline(w, q, k, v, qo - ko, args.cpu_seconds)
     print(json.dumps(out), flush=True)
 
 

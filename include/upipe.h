@@ -122,6 +122,46 @@ int upipe_attn_fwd(const void* q, const void* k, const void* v, void* o,
                    int U, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * One ring step of context-parallel attention (Section 2.2, Ring Attention
+ * with online softmax; Section 4, the Ulysses + Ring hybrid of USP that
+ * UPipe extends): attention of a query block against one key/value block
+ * that sits elsewhere in the sequence, returning the partial result that
+ * upipe_lse_merge folds into the running one.
+ *
+ *   q   bf16 [Sq, Hq, d]    queries at global positions q_offset + i
+ *   k   bf16 [Skv, Hkv, d]  keys at global positions kv_offset + j
+ *   v   bf16 [Skv, Hkv, d]  values
+ *   o   bf16 [Sq, Hq, d]    out: softmax-weighted values over the visible keys
+ *   lse fp32 [Hq, Sq]       out: natural-log log-sum-exp of the visible scaled
+ *                           scores
+ * With causal = 1, key j is visible to query i iff kv_offset + j <=
+ * q_offset + i; with causal = 0 every key is.  A row that sees no key gets
+ * o = 0 and lse = -inf (the empty set, neutral for the merge).  Head chunking
+ * by U as for upipe_attn_fwd; with Sq = Skv and q_offset = kv_offset this is
+ * upipe_attn_fwd.  |offsets| <= 2^62; workspace from
+ * upipe_attn_fwd_ring_workspace_size (0 for invalid shapes).
+ * ---------------------------------------------------------------------- */
+size_t upipe_attn_fwd_ring_workspace_size(int64_t Sq, int64_t Skv, int Hq, int Hkv,
+                                          int d, int U);
+int upipe_attn_fwd_ring(const void* q, const void* k, const void* v, void* o,
+                        float* lse, int64_t Sq, int64_t Skv, int64_t q_offset,
+                        int64_t kv_offset, int Hq, int Hkv, int d, int causal,
+                        int U, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Merge of two partial attention results over disjoint key sets (the
+ * online-softmax combination of successive ring steps, Section 2.2), in
+ * place on the running result:
+ *   lse' = log(exp(lse) + exp(lse_part))
+ *   o'   = exp(lse - lse') o + exp(lse_part - lse') o_part
+ * per row (s, h).  o, o_part bf16 [S, H, d]; lse, lse_part fp32 [H, S];
+ * lse = -inf marks an empty set.  Needs no workspace; d = 128.  Callers must
+ * not overlap o with o_part (or lse with lse_part).
+ * ---------------------------------------------------------------------- */
+int upipe_lse_merge(void* o, float* lse, const void* o_part, const float* lse_part,
+                    int64_t S, int H, int d, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * Attention backward (analytic gradient of the Section 2.1 definition,
  * Appendix A "Untied Ulysses (backward)": per-stage dQ, per-group dK/dV
  * accumulators that persist across stages).

@@ -53,7 +53,7 @@ Profiler& prof() {
 const char* const kFamilyNames[] = {
     "pack_rows",      "unpack_rows",   "rowdot_lse",     "attn_fwd",
     "attn_bwd_dkdv",  "attn_bwd_dq",   "gemm",           "gemm_wgrad",
-    "reduce_splitk",  "transpose_w",   "cast_f32_bf16",
+    "reduce_splitk",  "lse_merge",
 };
 const int kNumFamilies = sizeof(kFamilyNames) / sizeof(kFamilyNames[0]);
 
@@ -104,17 +104,22 @@ size_t Carver::take(size_t bytes) {
   return off;
 }
 
-AttnFwdPlan plan_attn_fwd(int64_t S, int Hq, int Hkv, int U) {
+AttnFwdPlan plan_attn_fwd_ring(int64_t Sq, int64_t Skv, int Hq, int Hkv, int U) {
   AttnFwdPlan p;
-  p.Sp = round_up(S, SEQ_PAD);
-  const size_t head = (size_t)p.Sp * HEAD_DIM * 2;
+  p.Sp = round_up(Sq, SEQ_PAD);
+  p.Skvp = round_up(Skv, SEQ_PAD);
+  const size_t qhead = (size_t)p.Sp * HEAD_DIM * 2, kvhead = (size_t)p.Skvp * HEAD_DIM * 2;
   Carver c;
-  p.Kp = c.take(Hkv * head);
-  p.Vp = c.take(Hkv * head);
-  p.Qc = c.take(U * head);
-  p.Oc = c.take(U * head);
+  p.Kp = c.take(Hkv * kvhead);
+  p.Vp = c.take(Hkv * kvhead);
+  p.Qc = c.take(U * qhead);
+  p.Oc = c.take(U * qhead);
   p.total = c.used;
   return p;
+}
+
+AttnFwdPlan plan_attn_fwd(int64_t S, int Hq, int Hkv, int U) {
+  return plan_attn_fwd_ring(S, S, Hq, Hkv, U);
 }
 
 AttnBwdPlan plan_attn_bwd(int64_t S, int Hq, int Hkv, int U) {
@@ -140,10 +145,10 @@ AttnBwdPlan plan_attn_bwd(int64_t S, int Hq, int Hkv, int U) {
 }
 
 // ------------------------------------------------------- attention paths
-int run_attn_fwd(const bf16* q, const bf16* k, const bf16* v, bf16* o,
-                 float* lse, int64_t S, int Hq, int Hkv, int causal, int U,
-                 char* ws, hipStream_t st) {
-  const AttnFwdPlan p = plan_attn_fwd(S, Hq, Hkv, U);
+int run_attn_fwd_ring(const bf16* q, const bf16* k, const bf16* v, bf16* o, float* lse,
+                      int64_t Sq, int64_t Skv, int64_t delta, int Hq, int Hkv, int causal,
+                      int U, char* ws, hipStream_t st) {
+  const AttnFwdPlan p = plan_attn_fwd_ring(Sq, Skv, Hq, Hkv, U);
   bf16* Kp = (bf16*)(ws + p.Kp);
   bf16* Vp = (bf16*)(ws + p.Vp);
   bf16* Qc = (bf16*)(ws + p.Qc);
@@ -152,14 +157,21 @@ int run_attn_fwd(const bf16* q, const bf16* k, const bf16* v, bf16* o,
   // Key/value heads: packed once, resident for every chunk (on one device
   // the GQA schedule needs each key/value head from its group's first stage
   // on, Section 4.1).
-  UPIPE_LAUNCH(kPackRows, st, launch_pack_rows(k, S, Hkv, 0, Hkv, p.Sp, Kp, st));
-  UPIPE_LAUNCH(kPackRows, st, launch_pack_rows(v, S, Hkv, 0, Hkv, p.Sp, Vp, st));
+  UPIPE_LAUNCH(kPackRows, st, launch_pack_rows(k, Skv, Hkv, 0, Hkv, p.Skvp, Kp, st));
+  UPIPE_LAUNCH(kPackRows, st, launch_pack_rows(v, Skv, Hkv, 0, Hkv, p.Skvp, Vp, st));
   for (int h0 = 0; h0 < Hq; h0 += U) {
-    UPIPE_LAUNCH(kPackRows, st, launch_pack_rows(q, S, Hq, h0, U, p.Sp, Qc, st));
-    UPIPE_LAUNCH(kAttnFwd, st, launch_attn_fwd(Qc, Kp, Vp, Oc, lse, S, p.Sp, U, h0, G, causal, st));
-    UPIPE_LAUNCH(kUnpackRows, st, launch_unpack_rows(Oc, S, Hq, h0, U, p.Sp, o, st));
+    UPIPE_LAUNCH(kPackRows, st, launch_pack_rows(q, Sq, Hq, h0, U, p.Sp, Qc, st));
+    UPIPE_LAUNCH(kAttnFwd, st, launch_attn_fwd(Qc, Kp, Vp, Oc, lse, Sq, p.Sp, Skv, p.Skvp, delta, U,
+                                               h0, G, causal, st));
+    UPIPE_LAUNCH(kUnpackRows, st, launch_unpack_rows(Oc, Sq, Hq, h0, U, p.Sp, o, st));
   }
   return UPIPE_OK;
+}
+
+int run_attn_fwd(const bf16* q, const bf16* k, const bf16* v, bf16* o,
+                 float* lse, int64_t S, int Hq, int Hkv, int causal, int U,
+                 char* ws, hipStream_t st) {
+  return run_attn_fwd_ring(q, k, v, o, lse, S, S, 0, Hq, Hkv, causal, U, ws, st);
 }
 
 int run_attn_bwd(const bf16* q, const bf16* k, const bf16* v, const bf16* o,
@@ -257,6 +269,52 @@ int upipe_attn_fwd(const void* q, const void* k, const void* v, void* o,
     if (ws_bytes < plan_attn_fwd(S, Hq, Hkv, U).total) return UPIPE_ERR_WORKSPACE;
     return run_attn_fwd((const bf16*)q, (const bf16*)k, (const bf16*)v, (bf16*)o, lse, S,
                         Hq, Hkv, causal, U, (char*)ws, stream);
+  } catch (...) {
+    return UPIPE_ERR_HIP;
+  }
+}
+
+size_t upipe_attn_fwd_ring_workspace_size(int64_t Sq, int64_t Skv, int Hq, int Hkv, int d, int U) {
+  if (check_attn_shape(Sq, Hq, Hkv, d, U) != UPIPE_OK) return 0;
+  if (check_attn_shape(Skv, Hq, Hkv, d, U) != UPIPE_OK) return 0;
+  return plan_attn_fwd_ring(Sq, Skv, Hq, Hkv, U).total;
+}
+
+int upipe_attn_fwd_ring(const void* q, const void* k, const void* v, void* o, float* lse,
+                        int64_t Sq, int64_t Skv, int64_t q_offset, int64_t kv_offset, int Hq,
+                        int Hkv, int d, int causal, int U, void* ws, size_t ws_bytes,
+                        hipStream_t stream) {
+  try {
+    int rc = check_attn_shape(Sq, Hq, Hkv, d, U);
+    if (rc != UPIPE_OK) return rc;
+    rc = check_attn_shape(Skv, Hq, Hkv, d, U);
+    if (rc != UPIPE_OK) return rc;
+    if (causal != 0 && causal != 1) return UPIPE_ERR_INVALID_ARG;
+    const int64_t lim = int64_t(1) << 62;
+    if (q_offset < -lim || q_offset > lim || kv_offset < -lim || kv_offset > lim)
+      return UPIPE_ERR_INVALID_ARG;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) ||
+        !aligned16(lse) || !aligned16(ws))
+      return UPIPE_ERR_INVALID_ARG;
+    if (ws_bytes < plan_attn_fwd_ring(Sq, Skv, Hq, Hkv, U).total) return UPIPE_ERR_WORKSPACE;
+    return run_attn_fwd_ring((const bf16*)q, (const bf16*)k, (const bf16*)v, (bf16*)o, lse, Sq,
+                             Skv, q_offset - kv_offset, Hq, Hkv, causal, U, (char*)ws, stream);
+  } catch (...) {
+    return UPIPE_ERR_HIP;
+  }
+}
+
+int upipe_lse_merge(void* o, float* lse, const void* o_part, const float* lse_part, int64_t S,
+                    int H, int d, hipStream_t stream) {
+  try {
+    if (S < 1 || H < 1) return UPIPE_ERR_INVALID_ARG;
+    if (d != HEAD_DIM) return UPIPE_ERR_UNSUPPORTED;
+    if (H > kMaxHeads || S > kMaxSeq) return UPIPE_ERR_UNSUPPORTED;
+    if (!aligned16(o) || !aligned16(lse) || !aligned16(o_part) || !aligned16(lse_part))
+      return UPIPE_ERR_INVALID_ARG;
+    UPIPE_LAUNCH(kLseMerge, stream,
+                 launch_lse_merge((bf16*)o, lse, (const bf16*)o_part, lse_part, S, H, stream));
+    return UPIPE_OK;
   } catch (...) {
     return UPIPE_ERR_HIP;
   }

@@ -25,8 +25,7 @@ enum Family {
   kGemm,
   kGemmWgrad,
   kReduceSplitk,
-  kTransposeW,
-  kCastF32,
+  kLseMerge,
 };
 
 // Records HIP events around one launch when profiling is on.
@@ -58,7 +57,8 @@ struct Carver {
 };
 
 struct AttnFwdPlan {
-  int64_t Sp = 0;
+  int64_t Sp = 0;     // query rows, padded
+  int64_t Skvp = 0;   // key/value rows, padded
   size_t Kp = 0, Vp = 0, Qc = 0, Oc = 0, total = 0;
 };
 
@@ -71,11 +71,15 @@ struct AttnBwdPlan {
 };
 
 AttnFwdPlan plan_attn_fwd(int64_t S, int Hq, int Hkv, int U);
+AttnFwdPlan plan_attn_fwd_ring(int64_t Sq, int64_t Skv, int Hq, int Hkv, int U);
 AttnBwdPlan plan_attn_bwd(int64_t S, int Hq, int Hkv, int U);
 
 int run_attn_fwd(const bf16* q, const bf16* k, const bf16* v, bf16* o,
                  float* lse, int64_t S, int Hq, int Hkv, int causal, int U,
                  char* ws, hipStream_t st);
+int run_attn_fwd_ring(const bf16* q, const bf16* k, const bf16* v, bf16* o, float* lse,
+                      int64_t Sq, int64_t Skv, int64_t delta, int Hq, int Hkv, int causal,
+                      int U, char* ws, hipStream_t st);
 int run_attn_bwd(const bf16* q, const bf16* k, const bf16* v, const bf16* o,
                  const float* lse, const bf16* dout, bf16* dq, bf16* dk,
                  bf16* dv, int64_t S, int Hq, int Hkv, int causal, int U,

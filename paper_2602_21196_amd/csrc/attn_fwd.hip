@@ -72,11 +72,17 @@ __device__ __forceinline__ float tile_probs4(const f32x16 (&st)[4], bf16x8 (&pf)
   return ls;
 }
 
+// One query block of one head against the key/value rows of its kv head.
+// Query row i (of Sq, padded to Sqp) may see key j (of Skv, padded to Skvp)
+// iff j <= i + delta (causal) -- delta = 0 and Skv = Sq is plain causal
+// self-attention; other offsets are one ring step of context-parallel
+// attention -- and always j < Skv.  A row that sees no key gets O = 0 and
+// lse = -inf, the neutral element of the log-sum-exp merge.
 template <bool CAUSAL>
 __global__ __launch_bounds__(512, 1) void attn_fwd_kernel(
     const bf16* __restrict__ Qc, const bf16* __restrict__ Kp, const bf16* __restrict__ Vp,
-    bf16* __restrict__ Oc, float* __restrict__ lse, int64_t S, int64_t Sp, int U, int h0, int G,
-    int nqb) {
+    bf16* __restrict__ Oc, float* __restrict__ lse, int Sq, int Sqp, int Skv, int Skvp, int delta,
+    int U, int h0, int G, int nqb) {
   __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
   const int t = threadIdx.x;
   const int lane = t & 63;
@@ -86,16 +92,14 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_kernel(
   const int qb = nqb - 1 - L / U;
   const int u = L % U;
   const int kvh = (h0 + u) / G;
-  const uint32_t Spv = (uint32_t)Sp;
-  const uint32_t q0 = (uint32_t)qb * BQ;
-  const uint32_t qw = q0 + 32 * w;          // first query row of this wave
-  const uint32_t myq = qw + r32;            // this lane's query row
-  const uint32_t Sv = (uint32_t)S;
-  const bool rows_ok = qw < Spv;            // the last block may hold 128 rows only
+  const int q0 = qb * BQ;
+  const int qw = q0 + 32 * w;               // first query row of this wave
+  const int myq = qw + r32;                 // this lane's query row
+  const bool rows_ok = qw < Sqp;            // the last block may hold 128 rows only
 
-  // One head's K and V rows [Sp][128], 32-bit addressed.
-  const buf_rsrc rk = make_rsrc(Kp + (int64_t)kvh * Sp * HEAD_DIM, Spv * 256u);
-  const buf_rsrc rv = make_rsrc(Vp + (int64_t)kvh * Sp * HEAD_DIM, Spv * 256u);
+  // One head's K and V rows [Skvp][128], 32-bit addressed.
+  const buf_rsrc rk = make_rsrc(Kp + (int64_t)kvh * Skvp * HEAD_DIM, (uint32_t)Skvp * 256u);
+  const buf_rsrc rv = make_rsrc(Vp + (int64_t)kvh * Skvp * HEAD_DIM, (uint32_t)Skvp * 256u);
   uint32_t offk[4], offv[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -106,8 +110,15 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_kernel(
     offv[i] = r * 256u + (((lane & 15) ^ tsw(r)) << 4);
   }
 
-  const int nst = CAUSAL ? (int)(min(q0 + BQ, Spv) / BKS) : (int)(Spv / BKS);
-  issue_tile(rk, rv, offk, offv, 0, smem, w);
+  // Stages of the workgroup (up to the last key its last row may see) and
+  // the leading ones holding a key visible to this wave.
+  const int max_st = Skvp / BKS;
+  const int nst = CAUSAL ? max(0, min(max_st, (min(q0 + BQ, Sqp) + delta + BKS - 1) / BKS)) : max_st;
+  const int nw = !rows_ok ? 0 : CAUSAL ? max(0, min(nst, (qw + 32 + delta + BKS - 1) / BKS)) : nst;
+  // Last visible key of this lane's row and of the wave's first row.
+  const int lim = CAUSAL ? min(myq + delta, Skv - 1) : Skv - 1;
+  const int lim_w = CAUSAL ? min(qw + delta, Skv - 1) : Skv - 1;
+  if (nst > 0) issue_tile(rk, rv, offk, offv, 0, smem, w);
 
   // Q^T B-operand fragments for the whole key loop: lane = query column,
   // k-group g covers head-dim [16s + 8g, 16s + 8g + 8).
@@ -117,7 +128,7 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_kernel(
 #pragma unroll
     for (int e = 0; e < 8; ++e) qf[s][e] = (bf16)0.f;
   if (rows_ok) {
-    const bf16* qp = Qc + ((int64_t)u * Sp + myq) * HEAD_DIM + 8 * g;
+    const bf16* qp = Qc + ((int64_t)u * Sqp + myq) * HEAD_DIM + 8 * g;
 #pragma unroll
     for (int s = 0; s < 8; ++s) qf[s] = *reinterpret_cast<const bf16x8*>(qp + 16 * s);
   }
@@ -127,20 +138,22 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_kernel(
   for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
     for (int i = 0; i < 16; ++i) oacc[dt][i] = 0.f;
-  float m_ref = -INFINITY;   // reference max of scaled scores, log2 domain
+  // Reference max of the scaled scores (log2 domain): a finite stand-in for
+  // -inf, so that a stage whose keys are all masked for a row leaves it at
+  // p = 0 rather than producing 0 * inf.
+  float m_ref = -1e30f;
   float l_run = 0.f;         // this lane's partial row sum
   const float sl2 = 1.4426950408889634f * 0.08838834764831845f;  // log2(e)/sqrt(128)
 
   for (int j = 0; j < nst; ++j) {
-    const uint32_t ks = (uint32_t)j * BKS;
+    const int ks = j * BKS;
     char* buf = smem + (j & 1) * STAGE;
     wait_vmem();
     __syncthreads();   // stage j landed for all waves; stage j-1's buffer is free
     if (j + 1 < nst) issue_tile(rk, rv, offk, offv, ks + BKS, smem + ((j + 1) & 1) * STAGE, w);
-    if (!rows_ok) continue;
-    if (CAUSAL && ks > qw + 31) continue;   // whole stage masked for this wave
+    if (j >= nw) continue;                  // whole stage masked for this wave
     {
-      const uint32_t kb = ks;
+      const int kb = ks;
       f32x16 st[4];
 #pragma unroll
       for (int tt = 0; tt < 4; ++tt)
@@ -151,16 +164,14 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_kernel(
 #pragma unroll
         for (int tt = 0; tt < 4; ++tt)
           st[tt] = mfma32x32x16(lds_read_b128(buf, swz256(32 * tt + r32, 2 * s + g)), qf[s], st[tt]);
-      // Mask: causal keys beyond the query row; keys past S when not causal.
-      const bool diag = CAUSAL ? (kb + BKS - 1 > qw) : (kb + BKS > Sv);
-      if (diag) {
+      // Mask keys past the row's last visible key (wave-uniform test first).
+      if (kb + BKS - 1 > lim_w) {
 #pragma unroll
         for (int tt = 0; tt < 4; ++tt)
 #pragma unroll
           for (int i = 0; i < 16; ++i) {
-            const uint32_t key = kb + 32 * tt + 8 * (i >> 2) + 4 * g + (i & 3);
-            const bool vis = CAUSAL ? (key <= myq) : (key < Sv);
-            if (!vis) st[tt][i] = -INFINITY;
+            const int key = kb + 32 * tt + 8 * (i >> 2) + 4 * g + (i & 3);
+            if (key > lim) st[tt][i] = -INFINITY;
           }
       }
       bf16x8 pf[4][2];
@@ -194,8 +205,8 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_kernel(
 
   if (!rows_ok) return;
   const float l_tot = l_run + __shfl_xor(l_run, 32);
-  const float inv = 1.f / l_tot;
-  bf16* op = Oc + ((int64_t)u * Sp + myq) * HEAD_DIM + 4 * g;
+  const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;   // no visible key: O = 0
+  bf16* op = Oc + ((int64_t)u * Sqp + myq) * HEAD_DIM + 4 * g;
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
@@ -205,23 +216,26 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_kernel(
       for (int b = 0; b < 4; ++b) ov[b] = (bf16)(oacc[dt][4 * a + b] * inv);
       *reinterpret_cast<bf16x4*>(op + 32 * dt + 8 * a) = ov;
     }
-  if (g == 0 && myq < Sv)
-    lse[(int64_t)(h0 + u) * S + myq] = (m_ref + __log2f(l_tot)) * 0.6931471805599453f;
+  if (g == 0 && myq < Sq)
+    lse[(int64_t)(h0 + u) * Sq + myq] =
+        l_tot > 0.f ? (m_ref + __log2f(l_tot)) * 0.6931471805599453f : -INFINITY;
 }
 
 }  // namespace
 
 hipError_t launch_attn_fwd(const bf16* Qc, const bf16* Kp, const bf16* Vp, bf16* Oc, float* lse,
-                           int64_t S, int64_t Sp, int U, int h0, int G, int causal,
-                           hipStream_t st) {
-  const int nqb = (int)((Sp + BQ - 1) / BQ);
+                           int64_t Sq, int64_t Sqp, int64_t Skv, int64_t Skvp, int64_t delta, int U,
+                           int h0, int G, int causal, hipStream_t st) {
+  const int nqb = (int)((Sqp + BQ - 1) / BQ);
+  // Offsets beyond either length change nothing: clamp into int range.
+  const int dl = (int)(delta < -Sq ? -Sq : delta > Skv ? Skv : delta);
   dim3 grid((unsigned)(nqb * U));
   if (causal)
-    hipLaunchKernelGGL(attn_fwd_kernel<true>, grid, dim3(512), 0, st, Qc, Kp, Vp, Oc, lse, S, Sp,
-                       U, h0, G, nqb);
+    hipLaunchKernelGGL(attn_fwd_kernel<true>, grid, dim3(512), 0, st, Qc, Kp, Vp, Oc, lse, (int)Sq,
+                       (int)Sqp, (int)Skv, (int)Skvp, dl, U, h0, G, nqb);
   else
-    hipLaunchKernelGGL(attn_fwd_kernel<false>, grid, dim3(512), 0, st, Qc, Kp, Vp, Oc, lse, S, Sp,
-                       U, h0, G, nqb);
+    hipLaunchKernelGGL(attn_fwd_kernel<false>, grid, dim3(512), 0, st, Qc, Kp, Vp, Oc, lse, (int)Sq,
+                       (int)Sqp, (int)Skv, (int)Skvp, dl, U, h0, G, nqb);
   return hipGetLastError();
 }
 

@@ -26,11 +26,19 @@ hipError_t launch_rowdot_lse(const bf16* a, int64_t a_row, int64_t a_head,
                              hipStream_t st);
 
 // ---- attention forward (attn_fwd.hip) ------------------------------------
-// Qc [U, Sp, d], Kp and Vp [Hkv, Sp, d] -> Oc [U, Sp, d] and lse rows
-// h0..h0+U-1 of the caller's [Hq, S] array.
+// Qc [U, Sqp, d], Kp and Vp [Hkv, Skvp, d] -> Oc [U, Sqp, d] and lse rows
+// h0..h0+U-1 of the caller's [Hq, Sq] array.  Query row i sees key j iff
+// j < Skv and (not causal or j <= i + delta); rows that see no key get O = 0,
+// lse = -inf.  Self-attention: Sq = Skv = S, delta = 0.
 hipError_t launch_attn_fwd(const bf16* Qc, const bf16* Kp, const bf16* Vp,
-                           bf16* Oc, float* lse, int64_t S, int64_t Sp, int U,
+                           bf16* Oc, float* lse, int64_t Sq, int64_t Sqp,
+                           int64_t Skv, int64_t Skvp, int64_t delta, int U,
                            int h0, int G, int causal, hipStream_t st);
+// In place, per row (s, h) of o [S, H, d] and lse [H, S]: fold the partial
+// result (o_p, lse_p) over a disjoint key set into (o, lse).
+hipError_t launch_lse_merge(bf16* o, float* lse, const bf16* o_p,
+                            const float* lse_p, int64_t S, int H,
+                            hipStream_t st);
 
 // ---- attention backward (attn_bwd.hip) -----------------------------------
 // lse_c below holds log2(e) * lse (the kernels evaluate exp2).

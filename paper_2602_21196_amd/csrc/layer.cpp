@@ -152,7 +152,7 @@ int run_layer_fwd(const bf16* x, const bf16* wqkv, const bf16* wo, bf16* y, bf16
                  gemm1(X, true, operand(wqkv + (int64_t)h0 * HEAD_DIM, ldw, U * HEAD_DIM, dm),
                        false, heads_epi(Qc, nullptr, U, Sp), GEMM_EPI_HEADS, Sp,
                        U * HEAD_DIM, dm, st));
-    UPIPE_LAUNCH(kAttnFwd, st, launch_attn_fwd(Qc, Kp, Vp, Oc, lse, S, Sp, U, h0, G, 1, st));
+    UPIPE_LAUNCH(kAttnFwd, st, launch_attn_fwd(Qc, Kp, Vp, Oc, lse, S, Sp, S, Sp, 0, U, h0, G, 1, st));
     UPIPE_LAUNCH(kUnpackRows, st, launch_unpack_rows(Oc, S, Hq, h0, U, Sp, o_saved, st));
     // Y32 (+)= O_c Wo_c; O_c read head-major, Wo rows [h0*d, (h0+U)*d).
     UPIPE_LAUNCH(kGemm, st,

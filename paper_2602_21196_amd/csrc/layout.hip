@@ -80,6 +80,53 @@ __global__ __launch_bounds__(256) void rowdot_lse_kernel(
   }
 }
 
+// Fold a partial softmax result over a disjoint key set (one ring step) into
+// the running one, per row (s, h) of o [S, H, d] and lse [H, S]:
+//   lse' = log(e^lse + e^lse_p),  o' = e^(lse - lse') o + e^(lse_p - lse') o_p,
+// with -inf marking an empty key set.  Sixteen lanes (16 bytes each) hold one
+// row; all of a row's lanes sit in one wave, and the new lse is computed from
+// the loaded values, so every lane has read the row's lse before any writes it.
+__global__ __launch_bounds__(256) void lse_merge_kernel(bf16* __restrict__ o, float* __restrict__ lse,
+                                                        const bf16* __restrict__ o_p,
+                                                        const float* __restrict__ lse_p, int64_t S,
+                                                        int H) {
+  const int64_t rows = S * H;
+  const int c = threadIdx.x & 15;
+  for (int64_t r = ((int64_t)blockIdx.x * 256 + threadIdx.x) >> 4; r < rows;
+       r += (int64_t)gridDim.x * 16) {
+    const int64_t s = r / H;
+    const int h = (int)(r % H);
+    const int64_t li = (int64_t)h * S + s;
+    const float la = lse[li], lb = lse_p[li];
+    const float m = fmaxf(la, lb);
+    float wa = 0.f, wb = 0.f, lnew = -INFINITY;
+    if (m != -INFINITY) {
+      wa = la == -INFINITY ? 0.f : __expf(la - m);
+      wb = lb == -INFINITY ? 0.f : __expf(lb - m);
+      const float tot = wa + wb;
+      lnew = m + __logf(tot);
+      wa /= tot;
+      wb /= tot;
+    }
+    const int64_t off = r * HEAD_DIM + 8 * c;
+    const bf16x8 a = *reinterpret_cast<const bf16x8*>(o + off);
+    const bf16x8 b = *reinterpret_cast<const bf16x8*>(o_p + off);
+    bf16x8 out;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) out[e] = (bf16)(wa * (float)a[e] + wb * (float)b[e]);
+    *reinterpret_cast<bf16x8*>(o + off) = out;
+    if (c == 0) lse[li] = lnew;
+  }
+}
+
+hipError_t launch_lse_merge(bf16* o, float* lse, const bf16* o_p, const float* lse_p, int64_t S,
+                            int H, hipStream_t st) {
+  const int64_t blocks = (S * H + 15) / 16;
+  hipLaunchKernelGGL(lse_merge_kernel, dim3((unsigned)(blocks < (1 << 20) ? blocks : (1 << 20))),
+                     dim3(256), 0, st, o, lse, o_p, lse_p, S, H);
+  return hipGetLastError();
+}
+
 hipError_t launch_pack_rows(const bf16* src, int64_t S, int H, int h0, int n,
                             int64_t Sp, bf16* dst, hipStream_t st) {
   dim3 grid((unsigned)(Sp / 64), (unsigned)n);

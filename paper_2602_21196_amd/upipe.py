@@ -42,6 +42,12 @@ _SIGNATURES = {
                               _c_void_p, _c_void_p, _c_void_p, _c_void_p,
                               _i64, _int, _int, _int, _int, _int,
                               _c_void_p, _size, _c_void_p]),
+    "upipe_attn_fwd_ring_workspace_size": (_size, [_i64, _i64, _int, _int, _int, _int]),
+    "upipe_attn_fwd_ring": (_int, [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _fptr,
+                                   _i64, _i64, _i64, _i64, _int, _int, _int, _int,
+                                   _int, _c_void_p, _size, _c_void_p]),
+    "upipe_lse_merge": (_int, [_c_void_p, _fptr, _c_void_p, _fptr, _i64, _int, _int,
+                               _c_void_p]),
     "upipe_layer_fwd": (_int, [_c_void_p, _c_void_p, _c_void_p, _c_void_p,
                                _c_void_p, _fptr, _i64, _int, _int, _int, _int,
                                _int, _c_void_p, _size, _c_void_p]),
@@ -133,6 +139,21 @@ def upipe_attn_bwd(q, k, v, o, lse, dout, dq, dk, dv, S, Hq, Hkv, d, causal,
                                 d, causal, U, ws, ws_bytes, stream)
 
 
+def upipe_attn_fwd_ring_workspace_size(Sq, Skv, Hq, Hkv, d, U):
+    return lib().upipe_attn_fwd_ring_workspace_size(Sq, Skv, Hq, Hkv, d, U)
+
+
+def upipe_attn_fwd_ring(q, k, v, o, lse, Sq, Skv, q_offset, kv_offset, Hq, Hkv,
+                        d, causal, U, ws, ws_bytes, stream):
+    return lib().upipe_attn_fwd_ring(q, k, v, o, lse, Sq, Skv, q_offset,
+                                     kv_offset, Hq, Hkv, d, causal, U, ws,
+                                     ws_bytes, stream)
+
+
+def upipe_lse_merge(o, lse, o_part, lse_part, S, H, d, stream):
+    return lib().upipe_lse_merge(o, lse, o_part, lse_part, S, H, d, stream)
+
+
 def upipe_layer_fwd(x, wqkv, wo, y, o_saved, lse_saved, S, d_model, Hq, Hkv,
                     d, U, ws, ws_bytes, stream):
     return lib().upipe_layer_fwd(x, wqkv, wo, y, o_saved, lse_saved, S,
@@ -220,6 +241,43 @@ def attn_fwd(q, k, v, causal=True, U=1, ws=None):
                         S, Hq, Hkv, d, int(causal), U, ws.data_ptr(),
                         ws.numel(), _stream())
     _check("upipe_attn_fwd", st)
+    return o, lse
+
+
+def attn_fwd_ring(q, k, v, q_offset, kv_offset, causal=True, U=1, ws=None):
+    """One ring step: o [Sq,Hq,d] bf16, lse [Hq,Sq] fp32 of q [Sq,Hq,d] (global
+    rows q_offset..) against k/v [Skv,Hkv,d] (global rows kv_offset..)."""
+    torch = _torch()
+    Sq, Hq, d = q.shape
+    Skv, Hkv = k.shape[0], k.shape[1]
+    need = upipe_attn_fwd_ring_workspace_size(Sq, Skv, Hq, Hkv, d, U)
+    if need == 0:
+        raise UpipeError("upipe_attn_fwd_ring_workspace_size", -1)
+    if ws is None:
+        ws = workspace(need, q.device)
+    o = torch.empty_like(q)
+    lse = torch.empty((Hq, Sq), dtype=torch.float32, device=q.device)
+    bf = torch.bfloat16
+    st = upipe_attn_fwd_ring(_ptr(q, bf, "q"), _ptr(k, bf, "k"), _ptr(v, bf, "v"),
+                             _ptr(o, bf, "o"), _ptr(lse, torch.float32, "lse"),
+                             Sq, Skv, int(q_offset), int(kv_offset), Hq, Hkv, d,
+                             int(causal), U, ws.data_ptr(), ws.numel(), _stream())
+    _check("upipe_attn_fwd_ring", st)
+    return o, lse
+
+
+def lse_merge(o, lse, o_part, lse_part):
+    """In place: fold (o_part [S,H,d], lse_part [H,S]) into (o, lse)."""
+    torch = _torch()
+    S, H, d = o.shape
+    if tuple(o_part.shape) != (S, H, d) or tuple(lse.shape) != (H, S) or \
+            tuple(lse_part.shape) != (H, S):
+        raise ValueError("lse_merge: o, o_part [S,H,d] and lse, lse_part [H,S]")
+    bf = torch.bfloat16
+    st = upipe_lse_merge(_ptr(o, bf, "o"), _ptr(lse, torch.float32, "lse"),
+                         _ptr(o_part, bf, "o_part"),
+                         _ptr(lse_part, torch.float32, "lse_part"), S, H, d, _stream())
+    _check("upipe_lse_merge", st)
     return o, lse
 
 

@@ -71,6 +71,48 @@ def test_argument_validation(fn):
     assert fn(ws_bytes=1024) == WS
 
 
+def _ring(**kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=FAKE, Sq=512, Skv=384, q_offset=1000,
+             kv_offset=200, Hq=4, Hkv=1, d=128, causal=1, U=1, ws=FAKE,
+             ws_bytes=1 << 40, stream=None)
+    a.update(kw)
+    return upipe.upipe_attn_fwd_ring(*a.values())
+
+
+def test_ring_step_validation_and_workspace():
+    INV, UNS, WS = -1, -2, -3
+    assert _ring(Sq=0) == INV
+    assert _ring(Skv=0) == INV
+    assert _ring(Hq=4, Hkv=3) == INV
+    assert _ring(U=3) == INV
+    assert _ring(d=64) == UNS
+    assert _ring(causal=2) == INV
+    assert _ring(q_offset=(1 << 62) + 1) == INV
+    assert _ring(kv_offset=-(1 << 62) - 1) == INV
+    assert _ring(k=None) == INV
+    assert _ring(lse=FAKE + 4) == INV
+    assert _ring(ws_bytes=1024) == WS
+    # K, V packed at the key length; Q, O chunk buffers at the query length
+    qh, kh = 512 * 128 * 2, 384 * 128 * 2
+    for U in (1, 2, 4):
+        assert upipe.upipe_attn_fwd_ring_workspace_size(512, 384, 4, 1, 128, U) == \
+            2 * kh + 2 * U * qh
+    # equal lengths: the plain forward's workspace
+    assert upipe.upipe_attn_fwd_ring_workspace_size(1000, 1000, 4, 2, 128, 2) == \
+        upipe.upipe_attn_fwd_workspace_size(1000, 4, 2, 128, 2)
+    assert upipe.upipe_attn_fwd_ring_workspace_size(512, 0, 4, 1, 128, 1) == 0
+
+
+def test_lse_merge_validation():
+    INV, UNS = -1, -2
+    m = upipe.upipe_lse_merge
+    assert m(FAKE, FAKE, FAKE, FAKE, 0, 4, 128, None) == INV
+    assert m(FAKE, FAKE, FAKE, FAKE, 16, 0, 128, None) == INV
+    assert m(FAKE, FAKE, FAKE, FAKE, 16, 4, 64, None) == UNS
+    assert m(None, FAKE, FAKE, FAKE, 16, 4, 128, None) == INV
+    assert m(FAKE, FAKE, FAKE + 2, FAKE, 16, 4, 128, None) == INV
+
+
 def test_workspace_sizes_follow_the_plan():
     S, d = 131072, 128
     Sp = S

@@ -55,6 +55,13 @@ WORKLOADS = {
     "llama8b_4m": Workload(
         "llama8b_4m", 4194304, 4, 1, 128, 4, (1,),
         note="Llama3-8B share at 4M tokens"),
+    "llama8b_ring": Workload(
+        "llama8b_ring", 32768, 4, 1, 128, 5, (1, 2, 4),
+        note="one ring step of the Llama3-8B share with the sequence split 4 "
+             "ways across ring ranks (Ulysses + Ring hybrid): a 32K query "
+             "block against the preceding 32K key/value block (all keys "
+             "visible), merged into the running result",
+        extra={"ring": True, "kv_len": 32768, "q_offset": 32768, "kv_offset": 0}),
 }
 
 
@@ -93,9 +100,35 @@ def layer_inputs(S, d_model, Hq, Hkv, d, seed, w_std=0.02):
     return x, wqkv, wo, dy
 
 
+def ring_inputs(w: Workload):
+    """q [S,Hq,d] (the query block), k, v [kv_len,Hkv,d] (the key block)."""
+    gen = torch.Generator(device="cpu").manual_seed(w.seed)
+    q = _draw(gen, (w.S, w.Hq, w.d))
+    k = _draw(gen, (w.extra["kv_len"], w.Hkv, w.d))
+    v = _draw(gen, (w.extra["kv_len"], w.Hkv, w.d))
+    return q, k, v
+
+
+def ring_pairs(Sq, Skv, delta, causal=True):
+    """Visible (query, key) pairs of one head in a ring step: query i sees
+    key j < Skv iff j <= i + delta (all keys when not causal)."""
+    if not causal:
+        return Sq * Skv
+    total = 0
+    lo = max(0, -delta)                      # first row seeing any key
+    full = max(lo, min(Sq, Skv - 1 - delta))  # rows < full see i + delta + 1 keys
+    n = full - lo
+    if n > 0:
+        total += n * (lo + delta + 1) + n * (n - 1) // 2
+    total += max(0, Sq - max(full, lo)) * Skv if Skv - 1 - delta < Sq else 0
+    return total
+
+
 def inputs_for(w: Workload):
     if w.is_layer:
         return layer_inputs(w.S, w.d_model, w.Hq, w.Hkv, w.d, w.seed)
+    if w.extra.get("ring"):
+        return ring_inputs(w)
     return attention_inputs(w.S, w.Hq, w.Hkv, w.d, w.seed)
 
 
