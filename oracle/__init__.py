@@ -13,6 +13,11 @@ definitions so that each function can be checked against the paper by eye:
 * ``layer``      -- the attention block around it: QKV projection,
   attention, output projection (Section 3.2 walk-through, Appendix A
   paragraphs on the forward and backward of the block).
+* ``ring``       -- one ring step of context-parallel attention (a query
+  block against a key/value block at another offset) and the log-sum-exp
+  merge of partial results (Section 2.2, Section 4 "Implementation").
+* ``rope``       -- rotary position embedding of queries and keys and its
+  inverse (Section 4 "Implementation", RoFormer's definition).
 * ``schedule``   -- the head-chunk plan: nu = H/U stages and the GQA
   out-of-order head schedule with its communication count (Section 4.1,
   "Grouped-Query Attention Scheduling"; Section 3.3 "Untied Ulysses").
@@ -25,4 +30,4 @@ than itself: closed forms, brute-force scalar loops, torch's fp64
 invariants and the values the paper prints.
 """
 
-from . import attention, layer, schedule, memory  # noqa: F401
+from . import attention, layer, memory, ring, rope, schedule  # noqa: F401

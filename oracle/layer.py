@@ -8,22 +8,28 @@ paragraphs "Untied Ulysses (forward)" / "(backward)"): the hidden states X
 are projected to Q, K, V, attention runs per head, the per-head outputs fill
 ``final_out`` and the output projection proj_o maps it back to d_model.
 
-Weight layout used here (no bias, no rotary embedding, no normalisation):
+Weight layout used here (no bias, no normalisation):
     x    [S, dm]
     wqkv [dm, (Hq + 2 Hkv) d]  columns = [Q heads | K heads | V heads],
                                each head a block of d consecutive columns
     wo   [Hq d, dm]            rows = the heads of final_out, in order
     y    [S, dm] = final_out.reshape(S, Hq d) @ wo
 
+Rotary embedding (optional, ``rope_base``): the projected Q and K heads are
+rotated at positions pos0 + s before attention (``oracle.rope``; the paper's
+Section 4 "Implementation" runs it fused and in place).  V is not rotated.
+
 Backward (chain rule on the same definition):
     dO    = dY wo^T              dWo   = final_out^T dY
-    dQ, dK, dV from the attention gradient
+    dQ, dK, dV from the attention gradient (with RoPE: with respect to the
+                  rotated Q, K, then turned back by the inverse rotation)
     dX    = [dQ|dK|dV] wqkv^T    dWqkv = X^T [dQ|dK|dV]
 """
 
 import numpy as np
 
 from . import attention
+from .rope import rope
 
 
 def split_qkv(qkv, Hq, Hkv, d):
@@ -34,19 +40,27 @@ def split_qkv(qkv, Hq, Hkv, d):
     return q, k, v
 
 
-def layer_fwd(x, wqkv, wo, Hq, Hkv, d, causal=True):
+def _rotate(t, S, rope_base, pos0, inverse=False):
+    if rope_base is None:
+        return t
+    return rope(t, pos0 + np.arange(S), rope_base, inverse)
+
+
+def layer_fwd(x, wqkv, wo, Hq, Hkv, d, causal=True, rope_base=None, pos0=0):
     """Returns (y [S, dm], final_out [S, Hq, d], lse [Hq, S])."""
     x = np.asarray(x, np.float64)
     wqkv = np.asarray(wqkv, np.float64)
     wo = np.asarray(wo, np.float64)
     S = x.shape[0]
     q, k, v = split_qkv(x @ wqkv, Hq, Hkv, d)
+    q = _rotate(q, S, rope_base, pos0)
+    k = _rotate(k, S, rope_base, pos0)
     o, lse = attention.attn_fwd(q, k, v, causal)
     y = o.reshape(S, Hq * d) @ wo
     return y, o, lse
 
 
-def layer_bwd(x, wqkv, wo, dy, Hq, Hkv, d, causal=True):
+def layer_bwd(x, wqkv, wo, dy, Hq, Hkv, d, causal=True, rope_base=None, pos0=0):
     """Returns (dx [S, dm], dwqkv [dm, (Hq+2Hkv)d], dwo [Hq d, dm])."""
     x = np.asarray(x, np.float64)
     wqkv = np.asarray(wqkv, np.float64)
@@ -54,10 +68,14 @@ def layer_bwd(x, wqkv, wo, dy, Hq, Hkv, d, causal=True):
     dy = np.asarray(dy, np.float64)
     S = x.shape[0]
     q, k, v = split_qkv(x @ wqkv, Hq, Hkv, d)
+    q = _rotate(q, S, rope_base, pos0)
+    k = _rotate(k, S, rope_base, pos0)
     o, _ = attention.attn_fwd(q, k, v, causal)
     do = (dy @ wo.T).reshape(S, Hq, d)
     dwo = o.reshape(S, Hq * d).T @ dy
     dq, dk, dv = attention.attn_bwd(q, k, v, do, causal)
+    dq = _rotate(dq, S, rope_base, pos0, inverse=True)
+    dk = _rotate(dk, S, rope_base, pos0, inverse=True)
     dqkv = np.concatenate([dq.reshape(S, -1), dk.reshape(S, -1),
                            dv.reshape(S, -1)], axis=1)
     dx = dqkv @ wqkv.T
@@ -65,7 +83,7 @@ def layer_bwd(x, wqkv, wo, dy, Hq, Hkv, d, causal=True):
     return dx, dwqkv, dwo
 
 
-def layer_fwd_rows(x, wqkv, wo, Hq, Hkv, d, rows):
+def layer_fwd_rows(x, wqkv, wo, Hq, Hkv, d, rows, rope_base=None, pos0=0):
     """y, final_out and lse at the listed rows only (causal).
 
     K and V are needed for every position (each row sees all earlier keys),
@@ -77,9 +95,11 @@ def layer_fwd_rows(x, wqkv, wo, Hq, Hkv, d, rows):
     rows = np.asarray(rows, np.int64)
     S = x.shape[0]
     kv = x @ wqkv[:, Hq * d:]
-    k = kv[:, :Hkv * d].reshape(S, Hkv, d)
+    k = _rotate(kv[:, :Hkv * d].reshape(S, Hkv, d), S, rope_base, pos0)
     v = kv[:, Hkv * d:].reshape(S, Hkv, d)
     qr = (x[rows] @ wqkv[:, :Hq * d]).reshape(len(rows), Hq, d)
+    if rope_base is not None:
+        qr = rope(qr, pos0 + rows, rope_base)
     # Place the sampled query rows at their own positions; other rows are
     # never read because each listed row only sees keys <= itself.
     q = np.zeros((S, Hq, d))
