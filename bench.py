@@ -180,9 +180,13 @@ def main():
         ws_f = upipe.workspace(upipe.upipe_layer_fwd_workspace_size(S, dm, Hq, Hkv, d, U), dev)
         ws_b = upipe.workspace(upipe.upipe_layer_bwd_workspace_size(S, dm, Hq, Hkv, d, U), dev)
 
+        rope_base = w.extra.get("rope_base", 0.0)
+
         def step():
-            y, o, lse = upipe.layer_fwd(x, wqkv, wo, Hq, Hkv, d, U=U, ws=ws_f)
-            upipe.layer_bwd(x, wqkv, wo, o, lse, dy, Hq, Hkv, d, U=U, ws=ws_b)
+            y, o, lse = upipe.layer_fwd(x, wqkv, wo, Hq, Hkv, d, U=U, ws=ws_f,
+                                        rope_base=rope_base)
+            upipe.layer_bwd(x, wqkv, wo, o, lse, dy, Hq, Hkv, d, U=U, ws=ws_b,
+                            rope_base=rope_base)
     else:
         q, k, v, do = W.attention_inputs(S, Hq, Hkv, d, w.seed)
         qd, kd, vd, dod = (t.to(dev) for t in (q, k, v, do))
@@ -238,7 +242,8 @@ def main():
            "data": "synthetic",
            "config": {"workload": w.name, "S": S, "Hq": Hq, "Hkv": Hkv,
                       "d": d, "U": U, "causal": True, "seed": w.seed,
-                      **({"d_model": w.d_model} if w.is_layer else {})},
+                      **({"d_model": w.d_model,
+                          "rope_base": w.extra.get("rope_base", 0.0)} if w.is_layer else {})},
            "frac_of_peak": round(value / PEAK_BF16_TFLOPS, 4),
            "roofline": roofline, "kernels": kernels}
 

@@ -180,6 +180,23 @@ int upipe_attn_bwd(const void* q, const void* k, const void* v, const void* o,
                    int U, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * Rotary position embedding (RoFormer), in place (Section 4 "Implementation":
+ * RoPE applied to queries and keys without an fp32 copy of them).
+ *
+ *   x   bf16 [S, H, d], rotated in place (fp32 arithmetic, one rounding)
+ *   pos0     position of row 0: row s sits at position pos0 + s
+ *   base     frequency base (e.g. 500000 for Llama 3, 1000000 for Qwen 3)
+ *   inverse  0: rotate; 1: rotate back (the transpose, for gradients)
+ * Head coordinates e and e + d/2 form pair e (0 <= e < d/2), turned by the
+ * angle (pos0 + s) * base^(-2e/d).  d = 128.  Angles are reduced in fp64, so
+ * positions up to 2^32 keep full accuracy: 0 <= pos0 and pos0 + S <= 2^32
+ * (UPIPE_ERR_UNSUPPORTED otherwise); base must be finite and > 0
+ * (UPIPE_ERR_INVALID_ARG).  S = 0 is a no-op.  Needs no workspace.
+ * ---------------------------------------------------------------------- */
+int upipe_rope(void* x, int64_t S, int H, int d, int64_t pos0, double base, int inverse,
+               hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * Attention block forward (Section 3.3: per stage, QKV projection of the
  * stage's heads, attention, output written into `final_out`; the output
  * projection is accumulated per chunk in fp32).  Always causal.
@@ -191,12 +208,17 @@ int upipe_attn_bwd(const void* q, const void* k, const void* v, const void* o,
  *   o_saved   bf16 [S, Hq, d]                    out: final_out (attention
  *                                                output, saved for backward)
  *   lse_saved fp32 [Hq, S]                       out: row log-sum-exp
+ *   rope_base  0: no rotary embedding; > 0: Q and K heads are rotated as by
+ *              upipe_rope(base = rope_base, pos0) inside the projection,
+ *              before their single rounding to bf16 (Section 4
+ *              "Implementation": in place, no fp32 copy, no extra pass)
+ *   pos0       position of row 0 (same limits as upipe_rope)
  * d_model must be a multiple of 128.
  * ---------------------------------------------------------------------- */
 int upipe_layer_fwd(const void* x, const void* wqkv, const void* wo, void* y,
                     void* o_saved, float* lse_saved, int64_t S, int d_model,
-                    int Hq, int Hkv, int d, int U, void* ws, size_t ws_bytes,
-                    hipStream_t stream);
+                    int Hq, int Hkv, int d, int U, double rope_base, int64_t pos0,
+                    void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * Attention block backward (Appendix A "Untied Ulysses (backward)"): per
@@ -206,6 +228,10 @@ int upipe_layer_fwd(const void* x, const void* wqkv, const void* wo, void* y,
  * recomputed from x (activation checkpointing keeps only x, final_out, lse).
  *
  *   x, wqkv, wo        as for upipe_layer_fwd
+ *   rope_base, pos0    as for upipe_layer_fwd (the same values): Q and K are
+ *                      recomputed rotated, and the gradients of the rotated
+ *                      Q and K are turned back by the inverse rotation
+ *                      before the projection gradients use them
  *   o_saved, lse_saved the forward's outputs for the same x and weights
  *   dy    bf16 [S, d_model]                 upstream gradient of y
  *   dx    bf16 [S, d_model]                 out
@@ -218,7 +244,8 @@ int upipe_layer_bwd(const void* x, const void* wqkv, const void* wo,
                     const void* o_saved, const float* lse_saved,
                     const void* dy, void* dx, void* dwqkv, void* dwo,
                     int64_t S, int d_model, int Hq, int Hkv, int d, int U,
-                    void* ws, size_t ws_bytes, hipStream_t stream);
+                    double rope_base, int64_t pos0, void* ws, size_t ws_bytes,
+                    hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * Kernel timing (measurement aid).  While enabled, every kernel the library

@@ -9,6 +9,8 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <cmath>
+
 #include <mutex>
 #include <new>
 #include <vector>
@@ -53,7 +55,7 @@ Profiler& prof() {
 const char* const kFamilyNames[] = {
     "pack_rows",      "unpack_rows",   "rowdot_lse",     "attn_fwd",
     "attn_bwd_dkdv",  "attn_bwd_dq",   "gemm",           "gemm_wgrad",
-    "reduce_splitk",  "lse_merge",
+    "reduce_splitk",  "lse_merge",     "rope",
 };
 const int kNumFamilies = sizeof(kFamilyNames) / sizeof(kFamilyNames[0]);
 
@@ -168,6 +170,15 @@ int run_attn_fwd_ring(const bf16* q, const bf16* k, const bf16* v, bf16* o, floa
   return UPIPE_OK;
 }
 
+int make_rope(double base, int64_t pos0, int64_t S, RopeArgs* out) {
+  *out = RopeArgs{0.0, 0, 0};
+  if (base == 0.0) return UPIPE_OK;
+  if (!(base > 0.0) || !std::isfinite(base)) return UPIPE_ERR_INVALID_ARG;
+  if (pos0 < 0 || pos0 > kMaxRopePos || S > kMaxRopePos - pos0) return UPIPE_ERR_UNSUPPORTED;
+  *out = RopeArgs{std::log2(base), pos0, 1};
+  return UPIPE_OK;
+}
+
 int run_attn_fwd(const bf16* q, const bf16* k, const bf16* v, bf16* o,
                  float* lse, int64_t S, int Hq, int Hkv, int causal, int U,
                  char* ws, hipStream_t st) {
@@ -200,10 +211,10 @@ int run_attn_bwd(const bf16* q, const bf16* k, const bf16* v, const bf16* o,
                                    h0, U, p.Sp, D, lse_c, st));
     UPIPE_LAUNCH(kAttnBwdDkdv, st,
                  launch_attn_bwd_dkdv(Qc, dOc, lse_c, D, Kp, Vp, dK32, dV32, dk, dv, S, p.Sp, U,
-                                      h0, G, Hkv, causal, st));
+                                      h0, G, Hkv, causal, RopeArgs{}, st));
     UPIPE_LAUNCH(kAttnBwdDq, st,
                  launch_attn_bwd_dq(Qc, dOc, lse_c, D, Kp, Vp, dQc, S, p.Sp, U, h0, G, causal,
-                                    st));
+                                    RopeArgs{}, st));
     UPIPE_LAUNCH(kUnpackRows, st, launch_unpack_rows(dQc, S, Hq, h0, U, p.Sp, dq, st));
   }
   return UPIPE_OK;
@@ -314,6 +325,25 @@ int upipe_lse_merge(void* o, float* lse, const void* o_part, const float* lse_pa
       return UPIPE_ERR_INVALID_ARG;
     UPIPE_LAUNCH(kLseMerge, stream,
                  launch_lse_merge((bf16*)o, lse, (const bf16*)o_part, lse_part, S, H, stream));
+    return UPIPE_OK;
+  } catch (...) {
+    return UPIPE_ERR_HIP;
+  }
+}
+
+int upipe_rope(void* x, int64_t S, int H, int d, int64_t pos0, double base, int inverse,
+               hipStream_t stream) {
+  try {
+    if (S < 0 || H < 1 || (inverse != 0 && inverse != 1) || base == 0.0)
+      return UPIPE_ERR_INVALID_ARG;
+    if (d != HEAD_DIM) return UPIPE_ERR_UNSUPPORTED;
+    if (H > kMaxHeads || S > kMaxSeq) return UPIPE_ERR_UNSUPPORTED;
+    RopeArgs r;
+    const int rc = make_rope(base, pos0, S, &r);
+    if (rc != UPIPE_OK) return rc;
+    if (!aligned16(x)) return UPIPE_ERR_INVALID_ARG;
+    if (S == 0) return UPIPE_OK;
+    UPIPE_LAUNCH(kRope, stream, launch_rope((bf16*)x, S, H, r, inverse, stream));
     return UPIPE_OK;
   } catch (...) {
     return UPIPE_ERR_HIP;

@@ -26,6 +26,7 @@ enum Family {
   kGemmWgrad,
   kReduceSplitk,
   kLseMerge,
+  kRope,
 };
 
 // Records HIP events around one launch when profiling is on.
@@ -47,6 +48,12 @@ class ProfScope {
   } while (0)
 
 bool aligned16(const void* p);
+// Rotary-embedding arguments from the ABI's (base, pos0) for rows 0..S-1:
+// base == 0 means no rotation; otherwise base must be finite and > 0
+// (UPIPE_ERR_INVALID_ARG) and positions pos0 .. pos0 + S - 1 must lie in
+// [0, kMaxRopePos) (UPIPE_ERR_UNSUPPORTED).
+constexpr int64_t kMaxRopePos = int64_t(1) << 32;
+int make_rope(double base, int64_t pos0, int64_t S, RopeArgs* out);
 int check_attn_shape(int64_t S, int Hq, int Hkv, int d, int U);
 bool group_split(int Hq, int Hkv, int U);
 

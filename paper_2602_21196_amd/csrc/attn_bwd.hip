@@ -199,13 +199,13 @@ __device__ __forceinline__ void pair_step(const char* buf, int base, uint32_t qb
   dvdk_products(fb, pf0, sf0, dva, dka);                                      // D
 }
 
-template <bool CAUSAL>
+template <bool CAUSAL, bool ROPE>
 __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(
     const bf16* __restrict__ Qc, const bf16* __restrict__ dOc, const float* __restrict__ lse_c,
     const float* __restrict__ Dc, const bf16* __restrict__ Kp, const bf16* __restrict__ Vp,
     float* __restrict__ dK32,
     float* __restrict__ dV32, bf16* __restrict__ dk, bf16* __restrict__ dv, int64_t S, int64_t Sp,
-    int U, int h0, int G, int Hkv) {
+    int U, int h0, int G, int Hkv, RopeArgs rope) {
   __shared__ __attribute__((aligned(1024))) char smem[2 * KV_STAGE];
   const int t = threadIdx.x;
   const int lane = t & 63;
@@ -312,6 +312,18 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(
   }
 
   if (last) {
+    if (ROPE) {   // dK was taken with respect to rotated keys: turn it back
+#pragma unroll
+      for (int dt = 0; dt < 2; ++dt) {
+        const double f = rope_turns_per_pos(32 * dt + r32, rope.log2_base);
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          float c, s;
+          cos_sin_turns(rope_turn(rope.pos0 + kw + 8 * (i >> 2) + 4 * g + (i & 3), f), c, s);
+          rope_pair(dka[dt], dka[dt + 2], i, c, s, true);
+        }
+      }
+    }
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
@@ -360,12 +372,12 @@ __device__ __forceinline__ void issue_kstage(buf_rsrc rk, buf_rsrc rv, const uin
   }
 }
 
-template <bool CAUSAL>
+template <bool CAUSAL, bool ROPE>
 __global__ __launch_bounds__(512, 1) void attn_bwd_dq_kernel(
     const bf16* __restrict__ Qc, const bf16* __restrict__ dOc, const float* __restrict__ lse_c,
     const float* __restrict__ Dc, const bf16* __restrict__ Kp, const bf16* __restrict__ Vp,
     bf16* __restrict__ dQc, int64_t S, int64_t Sp, int U, int h0,
-    int G, int nqb) {
+    int G, int nqb, RopeArgs rope) {
   __shared__ __attribute__((aligned(1024))) char smem[2 * DQ_STAGE];
   const int t = threadIdx.x;
   const int lane = t & 63;
@@ -471,6 +483,17 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_kernel(
   }
 
   if (!rows_ok) return;
+  if (ROPE) {   // dQ was taken with respect to rotated queries: turn it back
+#pragma unroll
+    for (int dt = 0; dt < 2; ++dt)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int e = 32 * dt + 8 * (i >> 2) + 4 * g + (i & 3);
+        float c, s;
+        cos_sin_turns(rope_turn(rope.pos0 + myq, rope_turns_per_pos(e, rope.log2_base)), c, s);
+        rope_pair(qacc[dt], qacc[dt + 2], i, c, s, true);
+      }
+  }
   bf16* op = dQc + ((int64_t)u * Sp + myq) * HEAD_DIM + 4 * g;
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt)
@@ -488,29 +511,39 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_kernel(
 hipError_t launch_attn_bwd_dkdv(const bf16* Qc, const bf16* dOc, const float* lse_c, const float* D,
                                 const bf16* Kp, const bf16* Vp, float* dK32, float* dV32, bf16* dk,
                                 bf16* dv, int64_t S, int64_t Sp, int U, int h0, int G, int Hkv,
-                                int causal, hipStream_t st) {
+                                int causal, RopeArgs rope, hipStream_t st) {
   const int kv_lo = h0 / G, kv_hi = (h0 + U - 1) / G;
   dim3 grid((unsigned)(Sp / 128), (unsigned)(kv_hi - kv_lo + 1));
-  if (causal)
-    hipLaunchKernelGGL(attn_bwd_dkdv_kernel<true>, grid, dim3(256), 0, st, Qc, dOc, lse_c, D, Kp,
-                       Vp, dK32, dV32, dk, dv, S, Sp, U, h0, G, Hkv);
-  else
-    hipLaunchKernelGGL(attn_bwd_dkdv_kernel<false>, grid, dim3(256), 0, st, Qc, dOc, lse_c, D, Kp,
-                       Vp, dK32, dV32, dk, dv, S, Sp, U, h0, G, Hkv);
+#define UPIPE_DKDV(C, R)                                                                      \
+  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<C, R>), grid, dim3(256), 0, st, Qc, dOc, lse_c, D, \
+                     Kp, Vp, dK32, dV32, dk, dv, S, Sp, U, h0, G, Hkv, rope)
+  if (causal) {
+    if (rope.on) UPIPE_DKDV(true, true);
+    else UPIPE_DKDV(true, false);
+  } else {
+    if (rope.on) UPIPE_DKDV(false, true);
+    else UPIPE_DKDV(false, false);
+  }
+#undef UPIPE_DKDV
   return hipGetLastError();
 }
 
 hipError_t launch_attn_bwd_dq(const bf16* Qc, const bf16* dOc, const float* lse_c, const float* D,
                               const bf16* Kp, const bf16* Vp, bf16* dQc, int64_t S, int64_t Sp,
-                              int U, int h0, int G, int causal, hipStream_t st) {
+                              int U, int h0, int G, int causal, RopeArgs rope, hipStream_t st) {
   const int nqb = (int)((Sp + DQ_BQ - 1) / DQ_BQ);
   dim3 grid((unsigned)(nqb * U));
-  if (causal)
-    hipLaunchKernelGGL(attn_bwd_dq_kernel<true>, grid, dim3(512), 0, st, Qc, dOc, lse_c, D, Kp, Vp,
-                       dQc, S, Sp, U, h0, G, nqb);
-  else
-    hipLaunchKernelGGL(attn_bwd_dq_kernel<false>, grid, dim3(512), 0, st, Qc, dOc, lse_c, D, Kp,
-                       Vp, dQc, S, Sp, U, h0, G, nqb);
+#define UPIPE_DQ(C, R)                                                                         \
+  hipLaunchKernelGGL((attn_bwd_dq_kernel<C, R>), grid, dim3(512), 0, st, Qc, dOc, lse_c, D, Kp, \
+                     Vp, dQc, S, Sp, U, h0, G, nqb, rope)
+  if (causal) {
+    if (rope.on) UPIPE_DQ(true, true);
+    else UPIPE_DQ(true, false);
+  } else {
+    if (rope.on) UPIPE_DQ(false, true);
+    else UPIPE_DQ(false, false);
+  }
+#undef UPIPE_DQ
   return hipGetLastError();
 }
 

@@ -114,4 +114,53 @@ __device__ __forceinline__ bf16x8 tr_operand(const char* tile, int k0, int n0, i
   return v;
 }
 
+// ---- rotary position embedding (RoFormer), head coordinate pairs (e, e + 64)
+// for e < 64: at sequence position p the pair turns by p * theta_e with
+// theta_e = base^(-e/64); the inverse (transpose) turns by the opposite angle.
+struct RopeArgs {
+  double log2_base;   // log2 of the frequency base
+  int64_t pos0;       // position of sequence row 0
+  int on;             // 0: no rotation
+};
+
+// theta_e / (2 pi): turns per position of pair e, in fp64.  Positions reach
+// 2^24, so the whole turns of p * theta_e are removed in fp64 before anything
+// is rounded to fp32.
+__device__ __forceinline__ double rope_turns_per_pos(int e, double log2_base) {
+  return exp2(-(double)e * log2_base * (1.0 / 64.0)) * 0.15915494309189535;
+}
+
+// Fractional part, in [-1/2, 1/2], of p * f turns.
+__device__ __forceinline__ float rope_turn(int64_t p, double f) {
+  const double r = (double)p * f;
+  return (float)(r - rint(r));
+}
+
+// cos(2 pi t), sin(2 pi t): v_cos_f32 / v_sin_f32 take their argument in
+// turns; t is first brought into [-1/2, 1/2].
+__device__ __forceinline__ void cos_sin_turns(float t, float& c, float& s) {
+  t -= rintf(t);
+  c = __builtin_amdgcn_cosf(t);
+  s = __builtin_amdgcn_sinf(t);
+}
+
+// Rotate the pair (a, b) by the angle whose cos / sin are (c, s); `inverse`
+// turns the other way.
+__device__ __forceinline__ void rope_pair(float& a, float& b, float c, float s, bool inverse) {
+  if (inverse) s = -s;
+  const float ra = a * c - b * s;
+  const float rb = b * c + a * s;
+  a = ra;
+  b = rb;
+}
+
+// The same on element i of two accumulator tiles.
+__device__ __forceinline__ void rope_pair(f32x16& a, f32x16& b, int i, float c, float s,
+                                          bool inverse) {
+  float x = a[i], y = b[i];
+  rope_pair(x, y, c, s, inverse);
+  a[i] = x;
+  b[i] = y;
+}
+
 }  // namespace upipe

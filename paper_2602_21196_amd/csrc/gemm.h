@@ -39,6 +39,11 @@ struct GemmEpilogue {
   bf16* dst_norm[2];
   int64_t n_split;
   int64_t Sp;
+  // Rotary embedding of the heads of the groups whose bit is set in
+  // rope_groups (bit g: group g), row m at position rope.pos0 + m, applied
+  // to the fp32 accumulators before rounding.
+  RopeArgs rope;
+  int rope_groups;
   // GEMM_EPI_ACC32: accumulators start at c32[m][n] (ldc) unless `first`;
   // the result goes to c32 unless `last`, else to out[m][n] (ldo) as bf16.
   // Rows >= m_store are neither read nor written.

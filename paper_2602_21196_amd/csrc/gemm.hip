@@ -16,7 +16,10 @@
 // Operands may be split into 128-wide blocks with their own stride (the
 // head-major chunk buffers [U][Sp][128]).
 //
-// Tile: 128 x 128 per workgroup, 4 waves as 2 x 2 of 64 x 64, BK = 128,
+// Tile: 128 x 128 per workgroup, 4 waves as 2 x 2 of 64 x 32+32 (wave column
+// half wn holds columns 32 wn + 64 nt + 0..31, nt = 0, 1: the coordinate pairs
+// (e, e + 64) of a 128-wide head sit in one lane, which the rotary embedding
+// of the head-major epilogue needs), BK = 128,
 // double-buffered (128 KB of LDS) except for the fp32-accumulating products.  The k loop runs in ascending order with
 // one fp32 accumulator chain per output element, so a product split over
 // several calls (k ranges accumulated through an fp32 buffer) is bitwise equal
@@ -122,7 +125,7 @@ __global__ __launch_bounds__(256, 3 - GemmStages<EPI>::N) void gemm_kernel(
     for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt) {
-        const int64_t n = n0 + 64 * wn + 32 * nt + r32;
+        const int64_t n = n0 + 32 * wn + 64 * nt + r32;
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const int64_t m = m0 + 64 * wm + 32 * mt + 8 * (i >> 2) + 4 * g + (i & 3);
@@ -164,7 +167,7 @@ __global__ __launch_bounds__(256, 3 - GemmStages<EPI>::N) void gemm_kernel(
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt) af[mt] = frag<AM>(bufA, 64 * wm + 32 * mt, ks, lane);
 #pragma unroll
-      for (int nt = 0; nt < 2; ++nt) bfr[nt] = frag<BMODE>(bufB, 64 * wn + 32 * nt, ks, lane);
+      for (int nt = 0; nt < 2; ++nt) bfr[nt] = frag<BMODE>(bufB, 32 * wn + 64 * nt, ks, lane);
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
@@ -172,13 +175,31 @@ __global__ __launch_bounds__(256, 3 - GemmStages<EPI>::N) void gemm_kernel(
     }
   }
 
-  // ---- epilogues.  Lane holds column n = n0 + 64wn + 32nt + r32 and rows
+  // ---- epilogues.  Lane holds column n = n0 + 32wn + 64nt + r32 and rows
   //      m = m0 + 64wm + 32mt + 8a + 4g + b for element i = 4a + b.
+  if (EPI == GEMM_EPI_HEADS && E.rope.on &&
+      ((E.rope_groups >> (n0 / 128 < E.n_split ? 0 : 1)) & 1)) {
+    // Pair (e, e + 64), e = 32wn + r32, of rows m: acc[mt][0][i], acc[mt][1][i].
+    // The turn of the first row of each 32-row block is reduced in fp64; the
+    // offsets 8a + b (< 28) add at most 28 theta_e / 2 pi turns in fp32.
+    const double f = rope_turns_per_pos(32 * wn + r32, E.rope.log2_base);
+    const float ff = (float)f;
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt) {
+      const float t0 = rope_turn(E.rope.pos0 + m0 + 64 * wm + 32 * mt + 4 * g, f);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        float c, s;
+        cos_sin_turns(fmaf((float)(8 * (i >> 2) + (i & 3)), ff, t0), c, s);
+        rope_pair(acc[mt][0], acc[mt][1], i, c, s, false);
+      }
+    }
+  }
 #pragma unroll
   for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
     for (int nt = 0; nt < 2; ++nt) {
-      const int64_t n = n0 + 64 * wn + 32 * nt + r32;
+      const int64_t n = n0 + 32 * wn + 64 * nt + r32;
       const int64_t mb = m0 + 64 * wm + 32 * mt;
       if (EPI == GEMM_EPI_HEADS) {
         const int64_t nb = n / 128, e = n % 128;

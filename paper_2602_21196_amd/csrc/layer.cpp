@@ -21,6 +21,11 @@
 //   dWk = x^T dK,  dWv = x^T dV
 // Every fp32 accumulator is carried across chunks in one fixed order, so all
 // outputs are bitwise identical for every chunk size U.
+// Rotary embedding (optional, Section 4 "Implementation"): Q_c and K are
+// rotated in the projection epilogue, on the fp32 accumulators, before they
+// are rounded and stored -- in place, with no extra pass or fp32 copy.  The
+// backward recomputes them the same way and turns dQ_c and dK back by the
+// inverse rotation in the attention-backward kernels' final writes.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -97,12 +102,16 @@ LayerBwdPlan plan_layer_bwd(int64_t S, int d_model, int Hq, int Hkv, int U) {
   return p;
 }
 
-GemmEpilogue heads_epi(bf16* n0, bf16* n1, int64_t n_split, int64_t Sp) {
+// Head-major outputs; `rope` rotates the heads of group 0 (Q, or K of K|V).
+GemmEpilogue heads_epi(bf16* n0, bf16* n1, int64_t n_split, int64_t Sp,
+                       RopeArgs rope = RopeArgs{}) {
   GemmEpilogue e{};
   e.dst_norm[0] = n0;
   e.dst_norm[1] = n1;
   e.n_split = n_split;
   e.Sp = Sp;
+  e.rope = rope;
+  e.rope_groups = rope.on ? 1 : 0;
   return e;
 }
 
@@ -129,8 +138,8 @@ hipError_t gemm1(const GemmOperand& A, bool ak, const GemmOperand& B, bool bk, G
 }  // namespace
 
 int run_layer_fwd(const bf16* x, const bf16* wqkv, const bf16* wo, bf16* y, bf16* o_saved,
-                  float* lse, int64_t S, int dm, int Hq, int Hkv, int U, char* ws,
-                  hipStream_t st) {
+                  float* lse, int64_t S, int dm, int Hq, int Hkv, int U, RopeArgs rope,
+                  char* ws, hipStream_t st) {
   const LayerFwdPlan p = plan_layer_fwd(S, dm, Hq, Hkv, U);
   const int64_t Sp = p.Sp, ldw = (int64_t)(Hq + 2 * Hkv) * HEAD_DIM;
   bf16* Kp = (bf16*)(ws + p.Kp);
@@ -143,14 +152,14 @@ int run_layer_fwd(const bf16* x, const bf16* wqkv, const bf16* wo, bf16* y, bf16
   // K | V = x [Wk | Wv], both head-major.
   UPIPE_LAUNCH(kGemm, st,
                gemm1(X, true, operand(wqkv + (int64_t)Hq * HEAD_DIM, ldw, 2 * Hkv * HEAD_DIM, dm),
-                     false, heads_epi(Kp, Vp, Hkv, Sp), GEMM_EPI_HEADS, Sp,
+                     false, heads_epi(Kp, Vp, Hkv, Sp, rope), GEMM_EPI_HEADS, Sp,
                      2 * Hkv * HEAD_DIM, dm, st));
   const int nu = Hq / U;
   for (int c = 0; c < nu; ++c) {
     const int h0 = c * U;
     UPIPE_LAUNCH(kGemm, st,
                  gemm1(X, true, operand(wqkv + (int64_t)h0 * HEAD_DIM, ldw, U * HEAD_DIM, dm),
-                       false, heads_epi(Qc, nullptr, U, Sp), GEMM_EPI_HEADS, Sp,
+                       false, heads_epi(Qc, nullptr, U, Sp, rope), GEMM_EPI_HEADS, Sp,
                        U * HEAD_DIM, dm, st));
     UPIPE_LAUNCH(kAttnFwd, st, launch_attn_fwd(Qc, Kp, Vp, Oc, lse, S, Sp, S, Sp, 0, U, h0, G, 1, st));
     UPIPE_LAUNCH(kUnpackRows, st, launch_unpack_rows(Oc, S, Hq, h0, U, Sp, o_saved, st));
@@ -166,7 +175,7 @@ int run_layer_fwd(const bf16* x, const bf16* wqkv, const bf16* wo, bf16* y, bf16
 
 int run_layer_bwd(const bf16* x, const bf16* wqkv, const bf16* wo, const bf16* o_saved,
                   const float* lse, const bf16* dy, bf16* dx, bf16* dwqkv, bf16* dwo, int64_t S,
-                  int dm, int Hq, int Hkv, int U, char* ws, hipStream_t st) {
+                  int dm, int Hq, int Hkv, int U, RopeArgs rope, char* ws, hipStream_t st) {
   const LayerBwdPlan p = plan_layer_bwd(S, dm, Hq, Hkv, U);
   const AttnBwdPlan& a = p.attn;
   char* ab = ws + p.attn_base;
@@ -209,7 +218,7 @@ int run_layer_bwd(const bf16* x, const bf16* wqkv, const bf16* wo, const bf16* o
   // Recompute K and V (head-major).
   UPIPE_LAUNCH(kGemm, st,
                gemm1(X, true, operand(wqkv + (int64_t)Hq * HEAD_DIM, ldw, 2 * kvw, dm), false,
-                     heads_epi(Kp, Vp, Hkv, Sp), GEMM_EPI_HEADS, Sp, 2 * kvw, dm,
+                     heads_epi(Kp, Vp, Hkv, Sp, rope), GEMM_EPI_HEADS, Sp, 2 * kvw, dm,
                      st));
   const int nu = Hq / U;
   for (int c = 0; c < nu; ++c) {
@@ -231,13 +240,13 @@ int run_layer_bwd(const bf16* x, const bf16* wqkv, const bf16* wo, const bf16* o
     // Q_c recomputed, head-major.
     UPIPE_LAUNCH(kGemm, st,
                  gemm1(X, true, operand(wqkv + (int64_t)h0 * HEAD_DIM, ldw, w, dm), false,
-                       heads_epi(Qc, nullptr, U, Sp), GEMM_EPI_HEADS, Sp, w, dm,
+                       heads_epi(Qc, nullptr, U, Sp, rope), GEMM_EPI_HEADS, Sp, w, dm,
                        st));
     UPIPE_LAUNCH(kAttnBwdDkdv, st,
                  launch_attn_bwd_dkdv(Qc, dOc, lse_c, D, Kp, Vp, dK32, dV32, dKb, dVb, S, Sp, U,
-                                      h0, G, Hkv, 1, st));
+                                      h0, G, Hkv, 1, rope, st));
     UPIPE_LAUNCH(kAttnBwdDq, st,
-                 launch_attn_bwd_dq(Qc, dOc, lse_c, D, Kp, Vp, dQc, S, Sp, U, h0, G, 1, st));
+                 launch_attn_bwd_dq(Qc, dOc, lse_c, D, Kp, Vp, dQc, S, Sp, U, h0, G, 1, rope, st));
     // dX32 (+)= dQ_c Wq_c^T (Wqkv rows are k-contiguous in the chunk's columns).
     UPIPE_LAUNCH(kGemm, st,
                  gemm1(operand(dQc, HEAD_DIM, S, w, HEAD_DIM, Sp * HEAD_DIM), true,
@@ -283,16 +292,21 @@ size_t upipe_layer_bwd_workspace_size(int64_t S, int d_model, int Hq, int Hkv, i
 
 int upipe_layer_fwd(const void* x, const void* wqkv, const void* wo, void* y, void* o_saved,
                     float* lse_saved, int64_t S, int d_model, int Hq, int Hkv, int d, int U,
-                    void* ws, size_t ws_bytes, hipStream_t stream) {
+                    double rope_base, int64_t pos0, void* ws, size_t ws_bytes,
+                    hipStream_t stream) {
   try {
     int rc = check_layer_shape(S, d_model, Hq, Hkv, d, U);
+    if (rc != UPIPE_OK) return rc;
+    RopeArgs rope;
+    rc = make_rope(rope_base, pos0, S, &rope);
     if (rc != UPIPE_OK) return rc;
     if (!aligned16(x) || !aligned16(wqkv) || !aligned16(wo) || !aligned16(y) ||
         !aligned16(o_saved) || !aligned16(lse_saved) || !aligned16(ws))
       return UPIPE_ERR_INVALID_ARG;
     if (ws_bytes < plan_layer_fwd(S, d_model, Hq, Hkv, U).total) return UPIPE_ERR_WORKSPACE;
     return run_layer_fwd((const bf16*)x, (const bf16*)wqkv, (const bf16*)wo, (bf16*)y,
-                         (bf16*)o_saved, lse_saved, S, d_model, Hq, Hkv, U, (char*)ws, stream);
+                         (bf16*)o_saved, lse_saved, S, d_model, Hq, Hkv, U, rope, (char*)ws,
+                         stream);
   } catch (...) {
     return UPIPE_ERR_HIP;
   }
@@ -300,10 +314,13 @@ int upipe_layer_fwd(const void* x, const void* wqkv, const void* wo, void* y, vo
 
 int upipe_layer_bwd(const void* x, const void* wqkv, const void* wo, const void* o_saved,
                     const float* lse_saved, const void* dy, void* dx, void* dwqkv, void* dwo,
-                    int64_t S, int d_model, int Hq, int Hkv, int d, int U, void* ws,
-                    size_t ws_bytes, hipStream_t stream) {
+                    int64_t S, int d_model, int Hq, int Hkv, int d, int U, double rope_base,
+                    int64_t pos0, void* ws, size_t ws_bytes, hipStream_t stream) {
   try {
     int rc = check_layer_shape(S, d_model, Hq, Hkv, d, U);
+    if (rc != UPIPE_OK) return rc;
+    RopeArgs rope;
+    rc = make_rope(rope_base, pos0, S, &rope);
     if (rc != UPIPE_OK) return rc;
     if (!aligned16(x) || !aligned16(wqkv) || !aligned16(wo) || !aligned16(o_saved) ||
         !aligned16(lse_saved) || !aligned16(dy) || !aligned16(dx) || !aligned16(dwqkv) ||
@@ -312,7 +329,8 @@ int upipe_layer_bwd(const void* x, const void* wqkv, const void* wo, const void*
     if (ws_bytes < plan_layer_bwd(S, d_model, Hq, Hkv, U).total) return UPIPE_ERR_WORKSPACE;
     return run_layer_bwd((const bf16*)x, (const bf16*)wqkv, (const bf16*)wo,
                          (const bf16*)o_saved, lse_saved, (const bf16*)dy, (bf16*)dx,
-                         (bf16*)dwqkv, (bf16*)dwo, S, d_model, Hq, Hkv, U, (char*)ws, stream);
+                         (bf16*)dwqkv, (bf16*)dwo, S, d_model, Hq, Hkv, U, rope, (char*)ws,
+                         stream);
   } catch (...) {
     return UPIPE_ERR_HIP;
   }

@@ -25,6 +25,7 @@ _i64 = ctypes.c_int64
 _int = ctypes.c_int
 _size = ctypes.c_size_t
 _fptr = ctypes.c_void_p
+_dbl = ctypes.c_double
 
 _SIGNATURES = {
     "upipe_status_string": (ctypes.c_char_p, [_int]),
@@ -48,12 +49,13 @@ _SIGNATURES = {
                                    _int, _c_void_p, _size, _c_void_p]),
     "upipe_lse_merge": (_int, [_c_void_p, _fptr, _c_void_p, _fptr, _i64, _int, _int,
                                _c_void_p]),
+    "upipe_rope": (_int, [_c_void_p, _i64, _int, _int, _i64, _dbl, _int, _c_void_p]),
     "upipe_layer_fwd": (_int, [_c_void_p, _c_void_p, _c_void_p, _c_void_p,
                                _c_void_p, _fptr, _i64, _int, _int, _int, _int,
-                               _int, _c_void_p, _size, _c_void_p]),
+                               _int, _dbl, _i64, _c_void_p, _size, _c_void_p]),
     "upipe_layer_bwd": (_int, [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _fptr,
                                _c_void_p, _c_void_p, _c_void_p, _c_void_p,
-                               _i64, _int, _int, _int, _int, _int,
+                               _i64, _int, _int, _int, _int, _int, _dbl, _i64,
                                _c_void_p, _size, _c_void_p]),
     "upipe_profile_enable": (_int, [_int]),
     "upipe_profile_reset": (_int, []),
@@ -154,17 +156,23 @@ def upipe_lse_merge(o, lse, o_part, lse_part, S, H, d, stream):
     return lib().upipe_lse_merge(o, lse, o_part, lse_part, S, H, d, stream)
 
 
+def upipe_rope(x, S, H, d, pos0, base, inverse, stream):
+    return lib().upipe_rope(x, S, H, d, pos0, base, inverse, stream)
+
+
 def upipe_layer_fwd(x, wqkv, wo, y, o_saved, lse_saved, S, d_model, Hq, Hkv,
-                    d, U, ws, ws_bytes, stream):
+                    d, U, rope_base, pos0, ws, ws_bytes, stream):
     return lib().upipe_layer_fwd(x, wqkv, wo, y, o_saved, lse_saved, S,
-                                 d_model, Hq, Hkv, d, U, ws, ws_bytes, stream)
+                                 d_model, Hq, Hkv, d, U, rope_base, pos0, ws,
+                                 ws_bytes, stream)
 
 
 def upipe_layer_bwd(x, wqkv, wo, o_saved, lse_saved, dy, dx, dwqkv, dwo, S,
-                    d_model, Hq, Hkv, d, U, ws, ws_bytes, stream):
+                    d_model, Hq, Hkv, d, U, rope_base, pos0, ws, ws_bytes,
+                    stream):
     return lib().upipe_layer_bwd(x, wqkv, wo, o_saved, lse_saved, dy, dx,
-                                 dwqkv, dwo, S, d_model, Hq, Hkv, d, U, ws,
-                                 ws_bytes, stream)
+                                 dwqkv, dwo, S, d_model, Hq, Hkv, d, U,
+                                 rope_base, pos0, ws, ws_bytes, stream)
 
 
 def upipe_profile_enable(on):
@@ -305,8 +313,19 @@ def attn_bwd(q, k, v, o, lse, dout, causal=True, U=1, ws=None):
     return dq, dk, dv
 
 
-def layer_fwd(x, wqkv, wo, Hq, Hkv, d=128, U=1, ws=None):
-    """y [S,dm] bf16, o_saved [S,Hq,d] bf16, lse_saved [Hq,S] fp32."""
+def rope(x, base, pos0=0, inverse=False):
+    """In place on x [S,H,d] bf16: rotary embedding at positions pos0 + s."""
+    torch = _torch()
+    S, H, d = x.shape
+    st = upipe_rope(_ptr(x, torch.bfloat16, "x"), S, H, d, int(pos0), float(base),
+                    int(bool(inverse)), _stream())
+    _check("upipe_rope", st)
+    return x
+
+
+def layer_fwd(x, wqkv, wo, Hq, Hkv, d=128, U=1, ws=None, rope_base=0.0, pos0=0):
+    """y [S,dm] bf16, o_saved [S,Hq,d] bf16, lse_saved [Hq,S] fp32.
+    rope_base > 0 rotates Q and K at positions pos0 + s."""
     torch = _torch()
     S, dm = x.shape
     need = upipe_layer_fwd_workspace_size(S, dm, Hq, Hkv, d, U)
@@ -322,14 +341,14 @@ def layer_fwd(x, wqkv, wo, Hq, Hkv, d=128, U=1, ws=None):
                          _ptr(wo, bf, "wo"), _ptr(y, bf, "y"),
                          _ptr(o, bf, "o_saved"),
                          _ptr(lse, torch.float32, "lse_saved"),
-                         S, dm, Hq, Hkv, d, U, ws.data_ptr(), ws.numel(),
-                         _stream())
+                         S, dm, Hq, Hkv, d, U, float(rope_base), int(pos0),
+                         ws.data_ptr(), ws.numel(), _stream())
     _check("upipe_layer_fwd", st)
     return y, o, lse
 
 
 def layer_bwd(x, wqkv, wo, o_saved, lse_saved, dy, Hq, Hkv, d=128, U=1,
-              ws=None):
+              ws=None, rope_base=0.0, pos0=0):
     """dx [S,dm], dwqkv [dm,(Hq+2Hkv)d], dwo [Hq d, dm], all bf16."""
     torch = _torch()
     S, dm = x.shape
@@ -347,7 +366,7 @@ def layer_bwd(x, wqkv, wo, o_saved, lse_saved, dy, Hq, Hkv, d=128, U=1,
                          _ptr(lse_saved, torch.float32, "lse_saved"),
                          _ptr(dy, bf, "dy"), _ptr(dx, bf, "dx"),
                          _ptr(dwqkv, bf, "dwqkv"), _ptr(dwo, bf, "dwo"),
-                         S, dm, Hq, Hkv, d, U, ws.data_ptr(), ws.numel(),
-                         _stream())
+                         S, dm, Hq, Hkv, d, U, float(rope_base), int(pos0),
+                         ws.data_ptr(), ws.numel(), _stream())
     _check("upipe_layer_bwd", st)
     return dx, dwqkv, dwo

@@ -162,4 +162,45 @@ def test_layer_entry_points_validate():
     assert upipe.upipe_layer_fwd_workspace_size(S, 500, 4, 1, 128, 1) == 0
     assert upipe.upipe_layer_fwd_workspace_size(S, dm, 4, 1, 64, 1) == 0
     assert upipe.upipe_layer_fwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, S, dm, 4,
-                                 1, 128, 3, FAKE, 1 << 40, None) == -1
+                                 1, 128, 3, 0.0, 0, FAKE, 1 << 40, None) == -1
+
+
+def _layer(fn, **kw):
+    a = dict(S=256, dm=512, Hq=4, Hkv=1, d=128, U=1, base=5e5, pos0=0)
+    a.update(kw)
+    if fn == "fwd":
+        return upipe.upipe_layer_fwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, a["S"], a["dm"],
+                                     a["Hq"], a["Hkv"], a["d"], a["U"], a["base"], a["pos0"],
+                                     FAKE, 0, None)
+    return upipe.upipe_layer_bwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                 a["S"], a["dm"], a["Hq"], a["Hkv"], a["d"], a["U"],
+                                 a["base"], a["pos0"], FAKE, 0, None)
+
+
+@pytest.mark.parametrize("fn", ["fwd", "bwd"])
+def test_layer_rope_arguments_validate(fn):
+    INV, UNS, WS = -1, -2, -3
+    assert _layer(fn) == WS                      # valid rotary arguments reach the size check
+    assert _layer(fn, base=0.0) == WS            # 0: no rotary embedding
+    assert _layer(fn, base=-1.0) == INV
+    assert _layer(fn, base=float("nan")) == INV
+    assert _layer(fn, base=float("inf")) == INV
+    assert _layer(fn, pos0=-1) == UNS
+    assert _layer(fn, pos0=(1 << 32) - 256) == WS   # last row at 2^32 - 1
+    assert _layer(fn, pos0=(1 << 32) - 255) == UNS
+
+
+def test_rope_entry_point_validates():
+    INV, UNS = -1, -2
+    r = upipe.upipe_rope
+    assert r(FAKE, 0, 4, 128, 0, 1e4, 0, None) == 0          # empty: nothing to do
+    assert r(FAKE, 16, 4, 64, 0, 1e4, 0, None) == UNS
+    assert r(FAKE, 16, 0, 128, 0, 1e4, 0, None) == INV
+    assert r(FAKE, -1, 4, 128, 0, 1e4, 0, None) == INV
+    assert r(FAKE, 16, 4, 128, 0, 0.0, 0, None) == INV       # no "off" for the standalone call
+    assert r(FAKE, 16, 4, 128, 0, -2.0, 0, None) == INV
+    assert r(FAKE, 16, 4, 128, 0, 1e4, 2, None) == INV
+    assert r(FAKE + 8, 16, 4, 128, 0, 1e4, 0, None) == INV   # misaligned
+    assert r(FAKE, 16, 4, 128, -5, 1e4, 0, None) == UNS
+    assert r(FAKE, 16, 4, 128, (1 << 32) - 15, 1e4, 0, None) == UNS
+    assert r(FAKE, 16, 65, 128, 0, 1e4, 0, None) == UNS

@@ -8,6 +8,7 @@ import torch
 import workloads as W
 from oracle import attention as A
 from oracle import layer as L
+from oracle import rope as R
 from tol import as64, assert_close
 
 pytestmark = pytest.mark.gpu
@@ -26,11 +27,11 @@ def _bits_equal(a, b):
     return torch.equal(a.view(torch.int32), b.view(torch.int32))
 
 
-def _run(x, wqkv, wo, dy, Hq, Hkv, U):
+def _run(x, wqkv, wo, dy, Hq, Hkv, U, rope_base=0.0):
     up = _upipe()
     xd, wd, wod, dyd = (t.to(DEV) for t in (x, wqkv, wo, dy))
-    y, o, lse = up.layer_fwd(xd, wd, wod, Hq, Hkv, U=U)
-    dx, dw, dwo = up.layer_bwd(xd, wd, wod, o, lse, dyd, Hq, Hkv, U=U)
+    y, o, lse = up.layer_fwd(xd, wd, wod, Hq, Hkv, U=U, rope_base=rope_base)
+    dx, dw, dwo = up.layer_bwd(xd, wd, wod, o, lse, dyd, Hq, Hkv, U=U, rope_base=rope_base)
     torch.cuda.synchronize()
     return [t.cpu() for t in (y, o, lse, dx, dw, dwo)]
 
@@ -89,13 +90,17 @@ def test_layer_llama_width_short_sequence():
 
 @pytest.mark.timeout(900)
 def test_llama8b_layer_share_sampled():
+    """The Llama3-8B layer share (S = 256K, d_model = 4096, RoPE with Llama 3's
+    base): bitwise equal across U; sampled rows and the key tail against the
+    oracle."""
     w = W.WORKLOADS["llama8b_layer"]
     S, dm, Hq, Hkv, d = w.S, w.d_model, w.Hq, w.Hkv, w.d
+    base = w.extra.get("rope_base")
     x, wqkv, wo, dy = W.layer_inputs(S, dm, Hq, Hkv, d, w.seed)
     outs = {}
     for U in w.U_sweep:
-        print(f"llama8b_layer S={S} U={U}", flush=True)
-        outs[U] = _run(x, wqkv, wo, dy, Hq, Hkv, U)
+        print(f"llama8b_layer S={S} U={U} rope_base={base}", flush=True)
+        outs[U] = _run(x, wqkv, wo, dy, Hq, Hkv, U, rope_base=base or 0.0)
     for U in w.U_sweep[1:]:
         for name, a, b in zip(NAMES, outs[1], outs[U]):
             assert _bits_equal(a, b), f"{name}: U=1 vs U={U}"
@@ -103,7 +108,7 @@ def test_llama8b_layer_share_sampled():
     x64, w64, wo64, dy64 = (as64(t) for t in (x, wqkv, wo, dy))
     rows = W.sample_rows(S, 128, w.seed)
     print("oracle sampled rows", flush=True)
-    y_r, o_r, lse_r = L.layer_fwd_rows(x64, w64, wo64, Hq, Hkv, d, rows)
+    y_r, o_r, lse_r = L.layer_fwd_rows(x64, w64, wo64, Hq, Hkv, d, rows, rope_base=base)
     assert_close("y rows", y[rows], y_r)
     assert_close("o rows", o[rows], o_r)
     assert_close("lse rows", lse[:, rows], lse_r)
@@ -112,10 +117,16 @@ def test_llama8b_layer_share_sampled():
     j0 = S - 256
     print("oracle key tail", flush=True)
     q, k, v = L.split_qkv(x64 @ w64, Hq, Hkv, d)
-    do = (dy64 @ wo64.T).reshape(S, Hq, d)
     tail = np.arange(j0, S)
+    if base is not None:   # attention sees rotated Q, K; their gradients turn back
+        q = R.rope(q, np.arange(S), base)
+        k = R.rope(k, np.arange(S), base)
+    do = (dy64 @ wo64.T).reshape(S, Hq, d)
     dq_t, _ = A.attn_bwd_rows(q, k, v, do, tail)
     dk_t, dv_t = A.attn_bwd_key_tail(q, k, v, do, j0)
+    if base is not None:
+        dq_t = R.rope(dq_t, tail, base, inverse=True)
+        dk_t = R.rope(dk_t, tail, base, inverse=True)
     dqkv = np.concatenate([dq_t.reshape(len(tail), -1), dk_t.reshape(len(tail), -1),
                            dv_t.reshape(len(tail), -1)], axis=1)
     assert_close("dx tail rows", dx[j0:], dqkv @ w64.T)

@@ -47,7 +47,9 @@ WORKLOADS = {
              "8/8 kv heads, S=128K"),
     "llama8b_layer": Workload(
         "llama8b_layer", 262144, 4, 1, 128, 2, (1, 2, 4), d_model=4096,
-        note="Llama3-8B per-GPU layer share: QKV slice, attention, O-proj"),
+        note="Llama3-8B per-GPU layer share: QKV slice with fused RoPE "
+             "(base 500000, Llama 3's), attention, O-proj",
+        extra={"rope_base": 500000.0}),
     "qwen32b_share": Workload(
         "qwen32b_share", 524288, 8, 1, 128, 3, (1, 2, 4, 8),
         note="Qwen3-32B-shaped per-GPU share: 64/8 query heads, 8/8 kv "
