@@ -44,6 +44,8 @@ def parse():
     p.add_argument("--no-sweep", action="store_true",
                    help="skip the per-U throughput/memory sweep")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--rope-base", type=float, default=None,
+                   help="layer workloads: rotary base (0 = none); default: the workload's")
     p.add_argument("--cpu-seconds", type=float, default=15.0,
                    help="target CPU time of the oracle sample")
     return p.parse_args()
@@ -180,7 +182,8 @@ def main():
         ws_f = upipe.workspace(upipe.upipe_layer_fwd_workspace_size(S, dm, Hq, Hkv, d, U), dev)
         ws_b = upipe.workspace(upipe.upipe_layer_bwd_workspace_size(S, dm, Hq, Hkv, d, U), dev)
 
-        rope_base = w.extra.get("rope_base", 0.0)
+        rope_base = (args.rope_base if args.rope_base is not None
+                     else w.extra.get("rope_base", 0.0))
 
         def step():
             y, o, lse = upipe.layer_fwd(x, wqkv, wo, Hq, Hkv, d, U=U, ws=ws_f,
@@ -243,7 +246,7 @@ def main():
            "config": {"workload": w.name, "S": S, "Hq": Hq, "Hkv": Hkv,
                       "d": d, "U": U, "causal": True, "seed": w.seed,
                       **({"d_model": w.d_model,
-                          "rope_base": w.extra.get("rope_base", 0.0)} if w.is_layer else {})},
+                          "rope_base": rope_base} if w.is_layer else {})},
            "frac_of_peak": round(value / PEAK_BF16_TFLOPS, 4),
            "roofline": roofline, "kernels": kernels}
 

@@ -211,7 +211,7 @@ int run_attn_bwd(const bf16* q, const bf16* k, const bf16* v, const bf16* o,
                                    h0, U, p.Sp, D, lse_c, st));
     UPIPE_LAUNCH(kAttnBwdDkdv, st,
                  launch_attn_bwd_dkdv(Qc, dOc, lse_c, D, Kp, Vp, dK32, dV32, dk, dv, S, p.Sp, U,
-                                      h0, G, Hkv, causal, RopeArgs{}, st));
+                                      h0, G, Hkv, causal, st));
     UPIPE_LAUNCH(kAttnBwdDq, st,
                  launch_attn_bwd_dq(Qc, dOc, lse_c, D, Kp, Vp, dQc, S, p.Sp, U, h0, G, causal,
                                     RopeArgs{}, st));

@@ -199,13 +199,13 @@ __device__ __forceinline__ void pair_step(const char* buf, int base, uint32_t qb
   dvdk_products(fb, pf0, sf0, dva, dka);                                      // D
 }
 
-template <bool CAUSAL, bool ROPE>
+template <bool CAUSAL>
 __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(
     const bf16* __restrict__ Qc, const bf16* __restrict__ dOc, const float* __restrict__ lse_c,
     const float* __restrict__ Dc, const bf16* __restrict__ Kp, const bf16* __restrict__ Vp,
     float* __restrict__ dK32,
     float* __restrict__ dV32, bf16* __restrict__ dk, bf16* __restrict__ dv, int64_t S, int64_t Sp,
-    int U, int h0, int G, int Hkv, RopeArgs rope) {
+    int U, int h0, int G, int Hkv) {
   __shared__ __attribute__((aligned(1024))) char smem[2 * KV_STAGE];
   const int t = threadIdx.x;
   const int lane = t & 63;
@@ -312,18 +312,6 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(
   }
 
   if (last) {
-    if (ROPE) {   // dK was taken with respect to rotated keys: turn it back
-#pragma unroll
-      for (int dt = 0; dt < 2; ++dt) {
-        const double f = rope_turns_per_pos(32 * dt + r32, rope.log2_base);
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          float c, s;
-          cos_sin_turns(rope_turn(rope.pos0 + kw + 8 * (i >> 2) + 4 * g + (i & 3), f), c, s);
-          rope_pair(dka[dt], dka[dt + 2], i, c, s, true);
-        }
-      }
-    }
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
@@ -511,20 +499,15 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_kernel(
 hipError_t launch_attn_bwd_dkdv(const bf16* Qc, const bf16* dOc, const float* lse_c, const float* D,
                                 const bf16* Kp, const bf16* Vp, float* dK32, float* dV32, bf16* dk,
                                 bf16* dv, int64_t S, int64_t Sp, int U, int h0, int G, int Hkv,
-                                int causal, RopeArgs rope, hipStream_t st) {
+                                int causal, hipStream_t st) {
   const int kv_lo = h0 / G, kv_hi = (h0 + U - 1) / G;
   dim3 grid((unsigned)(Sp / 128), (unsigned)(kv_hi - kv_lo + 1));
-#define UPIPE_DKDV(C, R)                                                                      \
-  hipLaunchKernelGGL((attn_bwd_dkdv_kernel<C, R>), grid, dim3(256), 0, st, Qc, dOc, lse_c, D, \
-                     Kp, Vp, dK32, dV32, dk, dv, S, Sp, U, h0, G, Hkv, rope)
-  if (causal) {
-    if (rope.on) UPIPE_DKDV(true, true);
-    else UPIPE_DKDV(true, false);
-  } else {
-    if (rope.on) UPIPE_DKDV(false, true);
-    else UPIPE_DKDV(false, false);
-  }
-#undef UPIPE_DKDV
+  if (causal)
+    hipLaunchKernelGGL(attn_bwd_dkdv_kernel<true>, grid, dim3(256), 0, st, Qc, dOc, lse_c, D, Kp,
+                       Vp, dK32, dV32, dk, dv, S, Sp, U, h0, G, Hkv);
+  else
+    hipLaunchKernelGGL(attn_bwd_dkdv_kernel<false>, grid, dim3(256), 0, st, Qc, dOc, lse_c, D, Kp,
+                       Vp, dK32, dV32, dk, dv, S, Sp, U, h0, G, Hkv);
   return hipGetLastError();
 }
 

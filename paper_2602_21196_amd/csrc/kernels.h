@@ -45,15 +45,16 @@ hipError_t launch_lse_merge(bf16* o, float* lse, const bf16* o_p,
 // Key/value gradients of the chunk's heads, accumulated in fp32 on top of
 // dK32/dV32 [Hkv, Sp, d] (read unless the chunk holds a group's first head),
 // written back there, or -- when the chunk holds the group's last head --
-// scaled and rounded into dk/dv bf16 [S, Hkv, d].  With rope.on, Q and K are
-// the rotated ones and dk is turned back by the inverse rotation of its row.
+// scaled and rounded into dk/dv bf16 [S, Hkv, d].
 hipError_t launch_attn_bwd_dkdv(const bf16* Qc, const bf16* dOc,
                                 const float* lse_c, const float* D,
                                 const bf16* Kp, const bf16* Vp, float* dK32,
                                 float* dV32, bf16* dk, bf16* dv, int64_t S,
                                 int64_t Sp, int U, int h0, int G, int Hkv,
-                                int causal, RopeArgs rope, hipStream_t st);
-// dQc [U, Sp, d] of the chunk's heads (turned back like dk with rope.on).
+                                int causal, hipStream_t st);
+// dQc [U, Sp, d] of the chunk's heads.  With rope.on, Q and K are the rotated
+// ones and dQ is turned back by the inverse rotation of its row before it is
+// rounded.
 hipError_t launch_attn_bwd_dq(const bf16* Qc, const bf16* dOc,
                               const float* lse_c, const float* D,
                               const bf16* Kp, const bf16* Vp, bf16* dQc, int64_t S, int64_t Sp, int U, int h0,

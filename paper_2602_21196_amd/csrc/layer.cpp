@@ -24,8 +24,9 @@
 // Rotary embedding (optional, Section 4 "Implementation"): Q_c and K are
 // rotated in the projection epilogue, on the fp32 accumulators, before they
 // are rounded and stored -- in place, with no extra pass or fp32 copy.  The
-// backward recomputes them the same way and turns dQ_c and dK back by the
-// inverse rotation in the attention-backward kernels' final writes.
+// backward recomputes them the same way and turns dQ_c back by the inverse
+// rotation in the dQ kernel's final write, and dK in one in-place pass after
+// the last chunk.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -244,7 +245,7 @@ int run_layer_bwd(const bf16* x, const bf16* wqkv, const bf16* wo, const bf16* o
                        st));
     UPIPE_LAUNCH(kAttnBwdDkdv, st,
                  launch_attn_bwd_dkdv(Qc, dOc, lse_c, D, Kp, Vp, dK32, dV32, dKb, dVb, S, Sp, U,
-                                      h0, G, Hkv, 1, rope, st));
+                                      h0, G, Hkv, 1, st));
     UPIPE_LAUNCH(kAttnBwdDq, st,
                  launch_attn_bwd_dq(Qc, dOc, lse_c, D, Kp, Vp, dQc, S, Sp, U, h0, G, 1, rope, st));
     // dX32 (+)= dQ_c Wq_c^T (Wqkv rows are k-contiguous in the chunk's columns).
@@ -258,6 +259,10 @@ int run_layer_bwd(const bf16* x, const bf16* wqkv, const bf16* wo, const bf16* o
                (int64_t)h0 * HEAD_DIM);
     if (rc != UPIPE_OK) return rc;
   }
+  // dK is the gradient with respect to the rotated keys: turn it back, in
+  // place (one bf16 pass over [S, Hkv, d]; kept out of the dK/dV kernel,
+  // whose register allocation is at its limit).
+  if (rope.on) UPIPE_LAUNCH(kRope, st, launch_rope(dKb, S, Hkv, rope, 1, st));
   // dX32 += dK Wk^T, then dX32 += dV Wv^T and round to dx.
   UPIPE_LAUNCH(kGemm, st,
                gemm1(operand(dKb, kvw, S, kvw), true,
