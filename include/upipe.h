@@ -197,9 +197,10 @@ int upipe_rope(void* x, int64_t S, int H, int d, int64_t pos0, double base, int 
                hipStream_t stream);
 
 /* ------------------------------------------------------------------------
- * Attention block forward (Section 3.3: per stage, QKV projection of the
- * stage's heads, attention, output written into `final_out`; the output
- * projection is accumulated per chunk in fp32).  Always causal.
+ * Attention block forward (Section 3.3, Appendix A "Untied Ulysses
+ * (forward)": per stage, QKV projection of the stage's heads, attention,
+ * output written into its slot of `final_out`; after the last stage the
+ * output projection y = final_out wo).  Always causal.
  *
  *   x         bf16 [S, d_model]                  hidden states
  *   wqkv      bf16 [d_model, (Hq + 2 Hkv) d]     columns [Q heads|K|V]
@@ -221,11 +222,13 @@ int upipe_layer_fwd(const void* x, const void* wqkv, const void* wo, void* y,
                     void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
- * Attention block backward (Appendix A "Untied Ulysses (backward)"): per
- * chunk, dO = dY wo_c^T, dWo_c = O_c^T dY, Q_c recomputed from x, attention
- * backward, dX += dQ_c wq_c^T, dWq_c = x^T dQ_c; after the last chunk
- * dX += dK wk^T + dV wv^T, dWk = x^T dK, dWv = x^T dV.  K and V are
- * recomputed from x (activation checkpointing keeps only x, final_out, lse).
+ * Attention block backward (Appendix A "Untied Ulysses (backward)"): the
+ * gradient of final_out, dY wo^T, is formed once and kept for the stage
+ * loop, and dWo = final_out^T dY; per chunk, Q_c is recomputed from x and the
+ * attention backward yields dQ_c and the running dK, dV sums; after the last
+ * chunk dX = [dQ | dK | dV] wqkv^T and dWqkv = x^T [dQ | dK | dV], each in
+ * one product.  K and V are recomputed from x (activation checkpointing
+ * keeps only x, final_out, lse).
  *
  *   x, wqkv, wo        as for upipe_layer_fwd
  *   rope_base, pos0    as for upipe_layer_fwd (the same values): Q and K are

@@ -210,8 +210,9 @@ int run_attn_bwd(const bf16* q, const bf16* k, const bf16* v, const bf16* o,
                                    o + h0 * HEAD_DIM, (int64_t)Hq * HEAD_DIM, HEAD_DIM, lse, S,
                                    h0, U, p.Sp, D, lse_c, st));
     UPIPE_LAUNCH(kAttnBwdDkdv, st,
-                 launch_attn_bwd_dkdv(Qc, dOc, lse_c, D, Kp, Vp, dK32, dV32, dk, dv, S, p.Sp, U,
-                                      h0, G, Hkv, causal, st));
+                 launch_attn_bwd_dkdv(Qc, dOc, lse_c, D, Kp, Vp, dK32, dV32, dk, dv,
+                                      (int64_t)Hkv * HEAD_DIM, HEAD_DIM, S, p.Sp, U, h0, G,
+                                      causal, st));
     UPIPE_LAUNCH(kAttnBwdDq, st,
                  launch_attn_bwd_dq(Qc, dOc, lse_c, D, Kp, Vp, dQc, S, p.Sp, U, h0, G, causal,
                                     RopeArgs{}, st));
@@ -343,7 +344,8 @@ int upipe_rope(void* x, int64_t S, int H, int d, int64_t pos0, double base, int 
     if (rc != UPIPE_OK) return rc;
     if (!aligned16(x)) return UPIPE_ERR_INVALID_ARG;
     if (S == 0) return UPIPE_OK;
-    UPIPE_LAUNCH(kRope, stream, launch_rope((bf16*)x, S, H, r, inverse, stream));
+    UPIPE_LAUNCH(kRope, stream,
+                 launch_rope((bf16*)x, S, H, (int64_t)H * HEAD_DIM, HEAD_DIM, r, inverse, stream));
     return UPIPE_OK;
   } catch (...) {
     return UPIPE_ERR_HIP;

@@ -205,7 +205,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(
     const float* __restrict__ Dc, const bf16* __restrict__ Kp, const bf16* __restrict__ Vp,
     float* __restrict__ dK32,
     float* __restrict__ dV32, bf16* __restrict__ dk, bf16* __restrict__ dv, int64_t S, int64_t Sp,
-    int U, int h0, int G, int Hkv) {
+    int U, int h0, int G, int64_t kv_row, int64_t kv_head) {
   __shared__ __attribute__((aligned(1024))) char smem[2 * KV_STAGE];
   const int t = threadIdx.x;
   const int lane = t & 63;
@@ -318,7 +318,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(
       for (int i = 0; i < 16; ++i) {
         const uint32_t key = kw + 8 * (i >> 2) + 4 * g + (i & 3);
         if (key < (uint64_t)S) {
-          const int64_t off = ((int64_t)key * Hkv + kvh) * HEAD_DIM + 32 * dt + r32;
+          const int64_t off = (int64_t)key * kv_row + kvh * kv_head + 32 * dt + r32;
           dk[off] = (bf16)(dka[dt][i] * kScale);
           dv[off] = (bf16)dva[dt][i];
         }
@@ -498,16 +498,16 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_kernel(
 
 hipError_t launch_attn_bwd_dkdv(const bf16* Qc, const bf16* dOc, const float* lse_c, const float* D,
                                 const bf16* Kp, const bf16* Vp, float* dK32, float* dV32, bf16* dk,
-                                bf16* dv, int64_t S, int64_t Sp, int U, int h0, int G, int Hkv,
-                                int causal, hipStream_t st) {
+                                bf16* dv, int64_t kv_row, int64_t kv_head, int64_t S, int64_t Sp,
+                                int U, int h0, int G, int causal, hipStream_t st) {
   const int kv_lo = h0 / G, kv_hi = (h0 + U - 1) / G;
   dim3 grid((unsigned)(Sp / 128), (unsigned)(kv_hi - kv_lo + 1));
   if (causal)
     hipLaunchKernelGGL(attn_bwd_dkdv_kernel<true>, grid, dim3(256), 0, st, Qc, dOc, lse_c, D, Kp,
-                       Vp, dK32, dV32, dk, dv, S, Sp, U, h0, G, Hkv);
+                       Vp, dK32, dV32, dk, dv, S, Sp, U, h0, G, kv_row, kv_head);
   else
     hipLaunchKernelGGL(attn_bwd_dkdv_kernel<false>, grid, dim3(256), 0, st, Qc, dOc, lse_c, D, Kp,
-                       Vp, dK32, dV32, dk, dv, S, Sp, U, h0, G, Hkv);
+                       Vp, dK32, dV32, dk, dv, S, Sp, U, h0, G, kv_row, kv_head);
   return hipGetLastError();
 }
 

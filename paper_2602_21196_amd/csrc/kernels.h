@@ -45,13 +45,15 @@ hipError_t launch_lse_merge(bf16* o, float* lse, const bf16* o_p,
 // Key/value gradients of the chunk's heads, accumulated in fp32 on top of
 // dK32/dV32 [Hkv, Sp, d] (read unless the chunk holds a group's first head),
 // written back there, or -- when the chunk holds the group's last head --
-// scaled and rounded into dk/dv bf16 [S, Hkv, d].
+// scaled and rounded into dk/dv bf16: row s of key/value head g at element
+// s * kv_row + g * kv_head (token-major [S, Hkv, d]: kv_row = Hkv * d,
+// kv_head = d; head-major [Hkv, Sp, d]: kv_row = d, kv_head = Sp * d).
 hipError_t launch_attn_bwd_dkdv(const bf16* Qc, const bf16* dOc,
                                 const float* lse_c, const float* D,
                                 const bf16* Kp, const bf16* Vp, float* dK32,
-                                float* dV32, bf16* dk, bf16* dv, int64_t S,
-                                int64_t Sp, int U, int h0, int G, int Hkv,
-                                int causal, hipStream_t st);
+                                float* dV32, bf16* dk, bf16* dv, int64_t kv_row,
+                                int64_t kv_head, int64_t S, int64_t Sp, int U,
+                                int h0, int G, int causal, hipStream_t st);
 // dQc [U, Sp, d] of the chunk's heads.  With rope.on, Q and K are the rotated
 // ones and dQ is turned back by the inverse rotation of its row before it is
 // rounded.
@@ -59,9 +61,10 @@ hipError_t launch_attn_bwd_dq(const bf16* Qc, const bf16* dOc,
                               const float* lse_c, const float* D,
                               const bf16* Kp, const bf16* Vp, bf16* dQc, int64_t S, int64_t Sp, int U, int h0,
                               int G, int causal, RopeArgs rope, hipStream_t st);
-// In place on x [S, H, d]: rotate every head of row s at position pos0 + s
-// (inverse: by the opposite angle).
-hipError_t launch_rope(bf16* x, int64_t S, int H, RopeArgs rope, int inverse,
-                       hipStream_t st);
+// In place: rotate every head h < H of row s < S, the 128 values at element
+// s * row + h * head of x, at position pos0 + s (inverse: by the opposite
+// angle).  Token-major [S, H, d]: row = H * d, head = d.
+hipError_t launch_rope(bf16* x, int64_t S, int H, int64_t row, int64_t head,
+                       RopeArgs rope, int inverse, hipStream_t st);
 
 }  // namespace upipe

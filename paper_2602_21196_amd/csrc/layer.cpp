@@ -6,21 +6,25 @@
 //     Q_c  = x Wq_c                          QKV projection slice
 //     O_c  = attention(Q_c, K, V)           flash forward, lse saved
 //     final_out[:, chunk] = O_c              (o_saved)
-//     Y32 += O_c Wo_c                        output-projection accumulation
-//   y = bf16(Y32)
+//   y = final_out Wo                         output projection, once
 // Backward (Appendix A "Untied Ulysses (backward)"), with K, V and Q_c
 // recomputed from x (activation checkpointing keeps x, final_out, lse):
+//   dFO   = dY Wo^T                          gradient of final_out, once,
+//                                            head-major, kept for the loop
+//   dWo   = final_out^T dY                   split-K over S, ordered sum
 //   per chunk c:
-//     dO_c  = dY Wo_c^T,   D = rowsum(dO_c * O_c)
-//     dWo_c = O_c^T dY                       split-K over S, ordered sum
+//     D     = rowsum(dFO_c * O_c)
 //     Q_c   = x Wq_c                         recompute
-//     dK, dV += ...,  dQ_c                   attention backward
-//     dX32 += dQ_c Wq_c^T                    full-size fp32 accumulator
-//     dWq_c = x^T dQ_c                       split-K over S
-//   dX32 += dK Wk^T;  dX32 += dV Wv^T;  dx = bf16(dX32)
-//   dWk = x^T dK,  dWv = x^T dV
-// Every fp32 accumulator is carried across chunks in one fixed order, so all
-// outputs are bitwise identical for every chunk size U.
+//     dK, dV += ...,  dQ_c                   attention backward; dQ_c lands
+//                                            in its heads' slots of dQKV
+//   dx    = [dQ | dK | dV] Wqkv^T            one product, bf16 out
+//   dWqkv = x^T [dQ | dK | dV]               split-K over S
+// The per-head results (dQ_c, the fp32 dK/dV carries taken in one fixed head
+// order) do not depend on U, and every product over heads runs once, so all
+// outputs are bitwise identical for every chunk size U.  On one GPU the
+// paper's per-stage accumulation of dX (a d_model-wide buffer updated by
+// every stage) becomes one product over the bf16 dQ of all heads, which is
+// smaller than that accumulator and reads nothing twice.
 // Rotary embedding (optional, Section 4 "Implementation"): Q_c and K are
 // rotated in the projection epilogue, on the fp32 accumulators, before they
 // are rounded and stored -- in place, with no extra pass or fp32 copy.  The
@@ -60,18 +64,20 @@ int64_t wgrad_split_len(int64_t S) {
 
 struct LayerFwdPlan {
   int64_t Sp = 0;
-  size_t Kp = 0, Vp = 0, Qc = 0, Oc = 0, Y32 = 0, total = 0;
-  bool y32 = false;
+  size_t Kp = 0, Vp = 0, Qc = 0, Oc = 0, total = 0;
 };
 
 struct LayerBwdPlan {
   int64_t Sp = 0, split_len = 0;
   int splits = 0;
-  AttnBwdPlan attn;            // offsets relative to `attn_base`
-  size_t attn_base = 0, dX32 = 0, dKb = 0, dVb = 0, partial = 0, total = 0;
+  bool carry = false;          // a key/value group spans several chunks
+  size_t Kp = 0, Vp = 0, dK32 = 0, dV32 = 0, Qc = 0, D = 0, lse_c = 0;
+  size_t dFO = 0, dQKV = 0, partial = 0, total = 0;
 };
 
 LayerFwdPlan plan_layer_fwd(int64_t S, int d_model, int Hq, int Hkv, int U) {
+  (void)d_model;
+  (void)Hq;
   LayerFwdPlan p;
   p.Sp = round_up(S, SEQ_PAD);
   const size_t head = (size_t)p.Sp * HEAD_DIM * 2;
@@ -80,8 +86,6 @@ LayerFwdPlan plan_layer_fwd(int64_t S, int d_model, int Hq, int Hkv, int U) {
   p.Vp = c.take(Hkv * head);
   p.Qc = c.take(U * head);
   p.Oc = c.take(U * head);
-  p.y32 = Hq / U > 1;
-  if (p.y32) p.Y32 = c.take((size_t)S * d_model * 4);
   p.total = c.used;
   return p;
 }
@@ -91,13 +95,24 @@ LayerBwdPlan plan_layer_bwd(int64_t S, int d_model, int Hq, int Hkv, int U) {
   p.Sp = round_up(S, SEQ_PAD);
   p.split_len = wgrad_split_len(S);
   p.splits = (int)((S + p.split_len - 1) / p.split_len);
-  p.attn = plan_attn_bwd(S, Hq, Hkv, U);
+  const size_t head = (size_t)p.Sp * HEAD_DIM * 2;
+  const size_t row32 = (size_t)p.Sp * 4;
   Carver c;
-  p.attn_base = c.take(p.attn.total);
-  p.dX32 = c.take((size_t)S * d_model * 4);
-  p.dKb = c.take((size_t)S * Hkv * HEAD_DIM * 2);
-  p.dVb = c.take((size_t)S * Hkv * HEAD_DIM * 2);
-  const int64_t widest = (U > Hkv ? U : Hkv) * (int64_t)HEAD_DIM;
+  p.Kp = c.take(Hkv * head);
+  p.Vp = c.take(Hkv * head);
+  p.carry = group_split(Hq, Hkv, U);
+  if (p.carry) {
+    p.dK32 = c.take(Hkv * head * 2);
+    p.dV32 = c.take(Hkv * head * 2);
+  }
+  p.Qc = c.take(U * head);
+  p.D = c.take(U * row32);
+  p.lse_c = c.take(U * row32);
+  p.dFO = c.take(Hq * head);
+  p.dQKV = c.take((Hq + 2 * Hkv) * head);
+  // Split-K partials of the larger weight gradient: dWqkv [d_model, (Hq +
+  // 2Hkv) d] or dWo [Hq d, d_model].
+  const int64_t widest = (int64_t)(Hq + 2 * Hkv) * HEAD_DIM;
   p.partial = c.take((size_t)p.splits * d_model * widest * 4);
   p.total = c.used;
   return p;
@@ -116,16 +131,14 @@ GemmEpilogue heads_epi(bf16* n0, bf16* n1, int64_t n_split, int64_t Sp,
   return e;
 }
 
-GemmEpilogue acc_epi(float* c32, int64_t ldc, bf16* out, int64_t ldo, int64_t m_store, bool first,
-                     bool last) {
+// bf16 result rows m < m_store into out[m * ldo + n], no fp32 carry.
+GemmEpilogue store_epi(bf16* out, int64_t ldo, int64_t m_store) {
   GemmEpilogue e{};
-  e.c32 = c32;
-  e.ldc = ldc;
   e.out = out;
   e.ldo = ldo;
   e.m_store = m_store;
-  e.first = first;
-  e.last = last;
+  e.first = 1;
+  e.last = 1;
   return e;
 }
 
@@ -143,34 +156,30 @@ int run_layer_fwd(const bf16* x, const bf16* wqkv, const bf16* wo, bf16* y, bf16
                   char* ws, hipStream_t st) {
   const LayerFwdPlan p = plan_layer_fwd(S, dm, Hq, Hkv, U);
   const int64_t Sp = p.Sp, ldw = (int64_t)(Hq + 2 * Hkv) * HEAD_DIM;
+  const int64_t qw = (int64_t)Hq * HEAD_DIM;
   bf16* Kp = (bf16*)(ws + p.Kp);
   bf16* Vp = (bf16*)(ws + p.Vp);
   bf16* Qc = (bf16*)(ws + p.Qc);
   bf16* Oc = (bf16*)(ws + p.Oc);
-  float* Y32 = p.y32 ? (float*)(ws + p.Y32) : nullptr;
   const int G = Hq / Hkv;
   const GemmOperand X = operand(x, dm, S, dm);
   // K | V = x [Wk | Wv], both head-major.
   UPIPE_LAUNCH(kGemm, st,
-               gemm1(X, true, operand(wqkv + (int64_t)Hq * HEAD_DIM, ldw, 2 * Hkv * HEAD_DIM, dm),
+               gemm1(X, true, operand(wqkv + qw, ldw, 2 * Hkv * HEAD_DIM, dm),
                      false, heads_epi(Kp, Vp, Hkv, Sp, rope), GEMM_EPI_HEADS, Sp,
                      2 * Hkv * HEAD_DIM, dm, st));
-  const int nu = Hq / U;
-  for (int c = 0; c < nu; ++c) {
-    const int h0 = c * U;
+  for (int h0 = 0; h0 < Hq; h0 += U) {
     UPIPE_LAUNCH(kGemm, st,
                  gemm1(X, true, operand(wqkv + (int64_t)h0 * HEAD_DIM, ldw, U * HEAD_DIM, dm),
                        false, heads_epi(Qc, nullptr, U, Sp, rope), GEMM_EPI_HEADS, Sp,
                        U * HEAD_DIM, dm, st));
     UPIPE_LAUNCH(kAttnFwd, st, launch_attn_fwd(Qc, Kp, Vp, Oc, lse, S, Sp, S, Sp, 0, U, h0, G, 1, st));
     UPIPE_LAUNCH(kUnpackRows, st, launch_unpack_rows(Oc, S, Hq, h0, U, Sp, o_saved, st));
-    // Y32 (+)= O_c Wo_c; O_c read head-major, Wo rows [h0*d, (h0+U)*d).
-    UPIPE_LAUNCH(kGemm, st,
-                 gemm1(operand(Oc, HEAD_DIM, S, U * HEAD_DIM, HEAD_DIM, Sp * HEAD_DIM), true,
-                       operand(wo + (int64_t)h0 * HEAD_DIM * dm, dm, dm, U * HEAD_DIM), false,
-                       acc_epi(Y32, dm, y, dm, S, c == 0, c == nu - 1), GEMM_EPI_ACC32, Sp, dm,
-                       U * HEAD_DIM, st));
   }
+  // y = final_out Wo.
+  UPIPE_LAUNCH(kGemm, st,
+               gemm1(operand(o_saved, qw, S, qw), true, operand(wo, dm, dm, qw), false,
+                     store_epi(y, dm, S), GEMM_EPI_ACC32, Sp, dm, qw, st));
   return UPIPE_OK;
 }
 
@@ -178,33 +187,32 @@ int run_layer_bwd(const bf16* x, const bf16* wqkv, const bf16* wo, const bf16* o
                   const float* lse, const bf16* dy, bf16* dx, bf16* dwqkv, bf16* dwo, int64_t S,
                   int dm, int Hq, int Hkv, int U, RopeArgs rope, char* ws, hipStream_t st) {
   const LayerBwdPlan p = plan_layer_bwd(S, dm, Hq, Hkv, U);
-  const AttnBwdPlan& a = p.attn;
-  char* ab = ws + p.attn_base;
   const int64_t Sp = p.Sp, ldw = (int64_t)(Hq + 2 * Hkv) * HEAD_DIM;
-  bf16* Kp = (bf16*)(ab + a.Kp);
-  bf16* Vp = (bf16*)(ab + a.Vp);
-  float* dK32 = a.carry ? (float*)(ab + a.dK32) : nullptr;
-  float* dV32 = a.carry ? (float*)(ab + a.dV32) : nullptr;
-  bf16* Qc = (bf16*)(ab + a.Qc);
-  bf16* dOc = (bf16*)(ab + a.dOc);
-  bf16* dQc = (bf16*)(ab + a.dQc);
-  float* D = (float*)(ab + a.D);
-  float* lse_c = (float*)(ab + a.lse_c);
-  float* dX32 = (float*)(ws + p.dX32);
-  bf16* dKb = (bf16*)(ws + p.dKb);
-  bf16* dVb = (bf16*)(ws + p.dVb);
+  const int64_t qw = (int64_t)Hq * HEAD_DIM, kvw = (int64_t)Hkv * HEAD_DIM;
+  const int64_t head = Sp * HEAD_DIM;   // elements of one head-major head
+  bf16* Kp = (bf16*)(ws + p.Kp);
+  bf16* Vp = (bf16*)(ws + p.Vp);
+  float* dK32 = p.carry ? (float*)(ws + p.dK32) : nullptr;
+  float* dV32 = p.carry ? (float*)(ws + p.dV32) : nullptr;
+  bf16* Qc = (bf16*)(ws + p.Qc);
+  float* D = (float*)(ws + p.D);
+  float* lse_c = (float*)(ws + p.lse_c);
+  bf16* dFO = (bf16*)(ws + p.dFO);
+  bf16* dQKV = (bf16*)(ws + p.dQKV);     // heads: dQ 0..Hq-1, dK Hq.., dV Hq+Hkv..
+  bf16* dKh = dQKV + (int64_t)Hq * head;
+  bf16* dVh = dKh + (int64_t)Hkv * head;
   float* partial = (float*)(ws + p.partial);
   const int G = Hq / Hkv;
-  const int64_t kvw = (int64_t)Hkv * HEAD_DIM;
+  const int64_t nqkv = (int64_t)(Hq + 2 * Hkv) * HEAD_DIM;
   const GemmOperand X = operand(x, dm, S, dm);
   const GemmOperand XT = operand(x, dm, dm, S);        // MN-major view: (m = col, k = s)
   const GemmOperand dY = operand(dy, dm, S, dm);
   const GemmOperand dYn = operand(dy, dm, dm, S);      // MN-major view: (n = col, k = s)
 
-  // Weight gradient C[M][N] = A^T-ish product over the sequence, split into
-  // fixed pieces and summed in order into out[m * ldo + col0 + n].
+  // Weight gradient C[M][N] = sum over s of A(m, s) B(n, s), split into fixed
+  // pieces of the sequence and summed in order into out[m * ldo + n].
   auto wgrad = [&](const GemmOperand& A, const GemmOperand& B, int64_t M, int64_t N, bf16* out,
-                   int64_t ldo, int64_t col0) -> int {
+                   int64_t ldo) -> int {
     GemmEpilogue e{};
     e.partial = partial;
     e.k_total = S;
@@ -212,71 +220,50 @@ int run_layer_bwd(const bf16* x, const bf16* wqkv, const bf16* wo, const bf16* o
                  launch_gemm(A, false, B, false, e, GEMM_EPI_PARTIAL, M, N, 0, p.split_len,
                              p.splits, st));
     UPIPE_LAUNCH(kReduceSplitk, st,
-                 launch_reduce_splitk(partial, p.splits, M, N, out, ldo, col0, st));
+                 launch_reduce_splitk(partial, p.splits, M, N, out, ldo, 0, st));
     return UPIPE_OK;
   };
 
-  // Recompute K and V (head-major).
+  // Recompute K and V (head-major, K rotated).
   UPIPE_LAUNCH(kGemm, st,
-               gemm1(X, true, operand(wqkv + (int64_t)Hq * HEAD_DIM, ldw, 2 * kvw, dm), false,
-                     heads_epi(Kp, Vp, Hkv, Sp, rope), GEMM_EPI_HEADS, Sp, 2 * kvw, dm,
-                     st));
-  const int nu = Hq / U;
-  for (int c = 0; c < nu; ++c) {
-    const int h0 = c * U;
+               gemm1(X, true, operand(wqkv + qw, ldw, 2 * kvw, dm), false,
+                     heads_epi(Kp, Vp, Hkv, Sp, rope), GEMM_EPI_HEADS, Sp, 2 * kvw, dm, st));
+  // dFO = dY Wo^T for every head, head-major (Wo rows are k-contiguous).
+  UPIPE_LAUNCH(kGemm, st,
+               gemm1(dY, true, operand(wo, dm, qw, dm), true, heads_epi(dFO, nullptr, Hq, Sp),
+                     GEMM_EPI_HEADS, Sp, qw, dm, st));
+  // dWo = final_out^T dY.
+  int rc = wgrad(operand(o_saved, qw, qw, S), dYn, qw, dm, dwo, dm);
+  if (rc != UPIPE_OK) return rc;
+  for (int h0 = 0; h0 < Hq; h0 += U) {
     const int64_t w = (int64_t)U * HEAD_DIM;
-    // dO_c = dY Wo_c^T (Wo rows of the chunk are k-contiguous).
-    UPIPE_LAUNCH(kGemm, st,
-                 gemm1(dY, true, operand(wo + (int64_t)h0 * HEAD_DIM * dm, dm, w, dm), true,
-                       heads_epi(dOc, nullptr, U, Sp), GEMM_EPI_HEADS, Sp, w, dm,
-                       st));
+    bf16* dOc = dFO + (int64_t)h0 * head;
+    bf16* dQc = dQKV + (int64_t)h0 * head;
     UPIPE_LAUNCH(kRowdotLse, st,
-                 launch_rowdot_lse(dOc, HEAD_DIM, Sp * HEAD_DIM, o_saved + (int64_t)h0 * HEAD_DIM,
-                                   (int64_t)Hq * HEAD_DIM, HEAD_DIM, lse, S, h0, U, Sp, D, lse_c,
-                                   st));
-    // dWo_c = O_c^T dY: rows (u, e) of the chunk, columns d_model.
-    int rc = wgrad(operand(o_saved + (int64_t)h0 * HEAD_DIM, (int64_t)Hq * HEAD_DIM, w, S), dYn,
-                   w, dm, dwo + (int64_t)h0 * HEAD_DIM * dm, dm, 0);
-    if (rc != UPIPE_OK) return rc;
-    // Q_c recomputed, head-major.
+                 launch_rowdot_lse(dOc, HEAD_DIM, head, o_saved + (int64_t)h0 * HEAD_DIM, qw,
+                                   HEAD_DIM, lse, S, h0, U, Sp, D, lse_c, st));
+    // Q_c recomputed, head-major, rotated.
     UPIPE_LAUNCH(kGemm, st,
                  gemm1(X, true, operand(wqkv + (int64_t)h0 * HEAD_DIM, ldw, w, dm), false,
-                       heads_epi(Qc, nullptr, U, Sp, rope), GEMM_EPI_HEADS, Sp, w, dm,
-                       st));
+                       heads_epi(Qc, nullptr, U, Sp, rope), GEMM_EPI_HEADS, Sp, w, dm, st));
     UPIPE_LAUNCH(kAttnBwdDkdv, st,
-                 launch_attn_bwd_dkdv(Qc, dOc, lse_c, D, Kp, Vp, dK32, dV32, dKb, dVb, S, Sp, U,
-                                      h0, G, Hkv, 1, st));
+                 launch_attn_bwd_dkdv(Qc, dOc, lse_c, D, Kp, Vp, dK32, dV32, dKh, dVh, HEAD_DIM,
+                                      head, S, Sp, U, h0, G, 1, st));
     UPIPE_LAUNCH(kAttnBwdDq, st,
                  launch_attn_bwd_dq(Qc, dOc, lse_c, D, Kp, Vp, dQc, S, Sp, U, h0, G, 1, rope, st));
-    // dX32 (+)= dQ_c Wq_c^T (Wqkv rows are k-contiguous in the chunk's columns).
-    UPIPE_LAUNCH(kGemm, st,
-                 gemm1(operand(dQc, HEAD_DIM, S, w, HEAD_DIM, Sp * HEAD_DIM), true,
-                       operand(wqkv + (int64_t)h0 * HEAD_DIM, ldw, dm, w), true,
-                       acc_epi(dX32, dm, dx, dm, S, c == 0, false), GEMM_EPI_ACC32, Sp, dm, w,
-                       st));
-    // dWq_c = x^T dQ_c.
-    rc = wgrad(XT, operand(dQc, HEAD_DIM, w, S, HEAD_DIM, Sp * HEAD_DIM), dm, w, dwqkv, ldw,
-               (int64_t)h0 * HEAD_DIM);
-    if (rc != UPIPE_OK) return rc;
   }
   // dK is the gradient with respect to the rotated keys: turn it back, in
-  // place (one bf16 pass over [S, Hkv, d]; kept out of the dK/dV kernel,
+  // place (one bf16 pass over [Hkv, S, d]; kept out of the dK/dV kernel,
   // whose register allocation is at its limit).
-  if (rope.on) UPIPE_LAUNCH(kRope, st, launch_rope(dKb, S, Hkv, rope, 1, st));
-  // dX32 += dK Wk^T, then dX32 += dV Wv^T and round to dx.
+  if (rope.on)
+    UPIPE_LAUNCH(kRope, st, launch_rope(dKh, S, Hkv, HEAD_DIM, head, rope, 1, st));
+  // dx = [dQ | dK | dV] Wqkv^T (head-major A; Wqkv rows are k-contiguous).
   UPIPE_LAUNCH(kGemm, st,
-               gemm1(operand(dKb, kvw, S, kvw), true,
-                     operand(wqkv + (int64_t)Hq * HEAD_DIM, ldw, dm, kvw), true,
-                     acc_epi(dX32, dm, dx, dm, S, false, false), GEMM_EPI_ACC32, Sp, dm, kvw, st));
-  UPIPE_LAUNCH(kGemm, st,
-               gemm1(operand(dVb, kvw, S, kvw), true,
-                     operand(wqkv + (int64_t)(Hq + Hkv) * HEAD_DIM, ldw, dm, kvw), true,
-                     acc_epi(dX32, dm, dx, dm, S, false, true), GEMM_EPI_ACC32, Sp, dm, kvw, st));
-  // dWk = x^T dK, dWv = x^T dV.
-  int rc = wgrad(XT, operand(dKb, kvw, kvw, S), dm, kvw, dwqkv, ldw, (int64_t)Hq * HEAD_DIM);
-  if (rc != UPIPE_OK) return rc;
-  rc = wgrad(XT, operand(dVb, kvw, kvw, S), dm, kvw, dwqkv, ldw, (int64_t)(Hq + Hkv) * HEAD_DIM);
-  return rc;
+               gemm1(operand(dQKV, HEAD_DIM, S, nqkv, HEAD_DIM, head), true,
+                     operand(wqkv, ldw, dm, nqkv), true, store_epi(dx, dm, S), GEMM_EPI_ACC32,
+                     Sp, dm, nqkv, st));
+  // dWqkv = x^T [dQ | dK | dV].
+  return wgrad(XT, operand(dQKV, HEAD_DIM, nqkv, S, HEAD_DIM, head), dm, nqkv, dwqkv, ldw);
 }
 
 }  // namespace upipe

@@ -127,12 +127,14 @@ hipError_t launch_lse_merge(bf16* o, float* lse, const bf16* o_p, const float* l
   return hipGetLastError();
 }
 
-// In-place rotary embedding of x [S, H, d] (the standalone form for callers
-// that project Q and K themselves; the layer fuses it into the projection).
+// In-place rotary embedding of H heads of S rows (the standalone form for
+// callers that project Q and K themselves, and the dK pass of the layer
+// backward; the layer's forward fuses it into the projection).
 // Thread = (row s, slice j of 8 pairs e = 8j..8j+7): the slice's frequencies
 // are formed once per thread, its 8 angles once per row, and every head of
 // the row is turned with them.  HBM-bound: one read and one write of x.
 __global__ __launch_bounds__(256) void rope_kernel(bf16* __restrict__ x, int64_t S, int H,
+                                                   int64_t row_stride, int64_t head_stride,
                                                    RopeArgs rope, int inverse) {
   const int j = threadIdx.x & 7;
   double f[8];
@@ -143,10 +145,10 @@ __global__ __launch_bounds__(256) void rope_kernel(bf16* __restrict__ x, int64_t
     float c[8], sn[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) cos_sin_turns(rope_turn(rope.pos0 + s, f[e]), c[e], sn[e]);
-    bf16* row = x + s * H * HEAD_DIM + 8 * j;
+    bf16* row = x + s * row_stride + 8 * j;
     for (int h = 0; h < H; ++h) {
-      bf16x8* pa = reinterpret_cast<bf16x8*>(row + (int64_t)h * HEAD_DIM);
-      bf16x8* pb = reinterpret_cast<bf16x8*>(row + (int64_t)h * HEAD_DIM + 64);
+      bf16x8* pa = reinterpret_cast<bf16x8*>(row + h * head_stride);
+      bf16x8* pb = reinterpret_cast<bf16x8*>(row + h * head_stride + 64);
       bf16x8 a = *pa, b = *pb;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
@@ -161,10 +163,11 @@ __global__ __launch_bounds__(256) void rope_kernel(bf16* __restrict__ x, int64_t
   }
 }
 
-hipError_t launch_rope(bf16* x, int64_t S, int H, RopeArgs rope, int inverse, hipStream_t st) {
+hipError_t launch_rope(bf16* x, int64_t S, int H, int64_t row, int64_t head, RopeArgs rope,
+                       int inverse, hipStream_t st) {
   const int64_t blocks = (S + 31) / 32;
   hipLaunchKernelGGL(rope_kernel, dim3((unsigned)(blocks < 8192 ? blocks : 8192)), dim3(256), 0,
-                     st, x, S, H, rope, inverse);
+                     st, x, S, H, row, head, rope, inverse);
   return hipGetLastError();
 }
 
