@@ -44,6 +44,9 @@ def parse():
     p.add_argument("--no-sweep", action="store_true",
                    help="skip the per-U throughput/memory sweep")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--checkpointing", choices=("selective", "full"), default="selective",
+                   help="layer workloads: keep the attention output for the backward "
+                        "(selective) or recompute it there (full)")
     p.add_argument("--rope-base", type=float, default=None,
                    help="layer workloads: rotary base (0 = none); default: the workload's")
     p.add_argument("--cpu-seconds", type=float, default=15.0,
@@ -185,9 +188,17 @@ def main():
         rope_base = (args.rope_base if args.rope_base is not None
                      else w.extra.get("rope_base", 0.0))
 
+        full_ac = args.checkpointing == "full"
+        # Tensors the forward leaves for the backward besides x and the
+        # weights: the attention output and its lse under selective
+        # checkpointing, nothing under full checkpointing.
+        kept_bytes = 0 if full_ac else 2 * S * Hq * d + 4 * Hq * S
+
         def step():
             y, o, lse = upipe.layer_fwd(x, wqkv, wo, Hq, Hkv, d, U=U, ws=ws_f,
                                         rope_base=rope_base)
+            if full_ac:
+                o = lse = None
             upipe.layer_bwd(x, wqkv, wo, o, lse, dy, Hq, Hkv, d, U=U, ws=ws_b,
                             rope_base=rope_base)
     else:
@@ -245,10 +256,17 @@ def main():
            "data": "synthetic",
            "config": {"workload": w.name, "S": S, "Hq": Hq, "Hkv": Hkv,
                       "d": d, "U": U, "causal": True, "seed": w.seed,
-                      **({"d_model": w.d_model,
-                          "rope_base": rope_base} if w.is_layer else {})},
+                      **({"d_model": w.d_model, "rope_base": rope_base,
+                          "checkpointing": args.checkpointing} if w.is_layer else {})},
            "frac_of_peak": round(value / PEAK_BF16_TFLOPS, 4),
            "roofline": roofline, "kernels": kernels}
+    if w.is_layer:
+        out["layer_memory_gb"] = {
+            "kept_for_backward": round(kept_bytes / 1e9, 4),
+            "fwd_workspace": round(upipe.upipe_layer_fwd_workspace_size(S, w.d_model, Hq, Hkv,
+                                                                         d, U) / 1e9, 4),
+            "bwd_workspace": round(upipe.upipe_layer_bwd_workspace_size(S, w.d_model, Hq, Hkv,
+                                                                         d, U) / 1e9, 4)}
 
     if not args.no_sweep and not w.is_layer:
         del ws_f, ws_b

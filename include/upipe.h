@@ -236,6 +236,11 @@ int upipe_layer_fwd(const void* x, const void* wqkv, const void* wo, void* y,
  *                      Q and K are turned back by the inverse rotation
  *                      before the projection gradients use them
  *   o_saved, lse_saved the forward's outputs for the same x and weights
+ *                      (selective checkpointing: the attention output is
+ *                      kept), or both NULL (full checkpointing: each
+ *                      chunk's attention forward is recomputed, bitwise
+ *                      equal to the forward's, at the cost of one more
+ *                      attention forward; the results are identical)
  *   dy    bf16 [S, d_model]                 upstream gradient of y
  *   dx    bf16 [S, d_model]                 out
  *   dwqkv bf16 [d_model, (Hq + 2 Hkv) d]    out

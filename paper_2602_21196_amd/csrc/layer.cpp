@@ -13,8 +13,10 @@
 //                                            head-major, kept for the loop
 //   dWo   = final_out^T dY                   split-K over S, ordered sum
 //   per chunk c:
-//     D     = rowsum(dFO_c * O_c)
 //     Q_c   = x Wq_c                         recompute
+//     (O_c, lse_c = attention(Q_c, K, V)     full checkpointing only: the
+//      dWo_c = O_c^T dY)                     attention output was not kept
+//     D     = rowsum(dFO_c * O_c)
 //     dK, dV += ...,  dQ_c                   attention backward; dQ_c lands
 //                                            in its heads' slots of dQKV
 //   dx    = [dQ | dK | dV] Wqkv^T            one product, bf16 out
@@ -72,6 +74,7 @@ struct LayerBwdPlan {
   int splits = 0;
   bool carry = false;          // a key/value group spans several chunks
   size_t Kp = 0, Vp = 0, dK32 = 0, dV32 = 0, Qc = 0, D = 0, lse_c = 0;
+  size_t Oc = 0, lse_r = 0;    // recomputed attention output (full checkpointing)
   size_t dFO = 0, dQKV = 0, partial = 0, total = 0;
 };
 
@@ -108,6 +111,8 @@ LayerBwdPlan plan_layer_bwd(int64_t S, int d_model, int Hq, int Hkv, int U) {
   p.Qc = c.take(U * head);
   p.D = c.take(U * row32);
   p.lse_c = c.take(U * row32);
+  p.Oc = c.take(U * head);
+  p.lse_r = c.take((size_t)Hq * S * 4);
   p.dFO = c.take(Hq * head);
   p.dQKV = c.take((Hq + 2 * Hkv) * head);
   // Split-K partials of the larger weight gradient: dWqkv [d_model, (Hq +
@@ -197,6 +202,9 @@ int run_layer_bwd(const bf16* x, const bf16* wqkv, const bf16* wo, const bf16* o
   bf16* Qc = (bf16*)(ws + p.Qc);
   float* D = (float*)(ws + p.D);
   float* lse_c = (float*)(ws + p.lse_c);
+  bf16* Oc = (bf16*)(ws + p.Oc);
+  float* lse_r = (float*)(ws + p.lse_r);
+  const bool recompute = o_saved == nullptr;   // full checkpointing: no saved output
   bf16* dFO = (bf16*)(ws + p.dFO);
   bf16* dQKV = (bf16*)(ws + p.dQKV);     // heads: dQ 0..Hq-1, dK Hq.., dV Hq+Hkv..
   bf16* dKh = dQKV + (int64_t)Hq * head;
@@ -232,20 +240,36 @@ int run_layer_bwd(const bf16* x, const bf16* wqkv, const bf16* wo, const bf16* o
   UPIPE_LAUNCH(kGemm, st,
                gemm1(dY, true, operand(wo, dm, qw, dm), true, heads_epi(dFO, nullptr, Hq, Sp),
                      GEMM_EPI_HEADS, Sp, qw, dm, st));
-  // dWo = final_out^T dY.
-  int rc = wgrad(operand(o_saved, qw, qw, S), dYn, qw, dm, dwo, dm);
-  if (rc != UPIPE_OK) return rc;
+  int rc;
+  if (!recompute) {   // dWo = final_out^T dY from the kept final_out
+    rc = wgrad(operand(o_saved, qw, qw, S), dYn, qw, dm, dwo, dm);
+    if (rc != UPIPE_OK) return rc;
+  }
   for (int h0 = 0; h0 < Hq; h0 += U) {
     const int64_t w = (int64_t)U * HEAD_DIM;
     bf16* dOc = dFO + (int64_t)h0 * head;
     bf16* dQc = dQKV + (int64_t)h0 * head;
-    UPIPE_LAUNCH(kRowdotLse, st,
-                 launch_rowdot_lse(dOc, HEAD_DIM, head, o_saved + (int64_t)h0 * HEAD_DIM, qw,
-                                   HEAD_DIM, lse, S, h0, U, Sp, D, lse_c, st));
     // Q_c recomputed, head-major, rotated.
     UPIPE_LAUNCH(kGemm, st,
                  gemm1(X, true, operand(wqkv + (int64_t)h0 * HEAD_DIM, ldw, w, dm), false,
                        heads_epi(Qc, nullptr, U, Sp, rope), GEMM_EPI_HEADS, Sp, w, dm, st));
+    if (recompute) {
+      // The chunk's attention output and lse again (the same kernel on the
+      // same operands: bitwise what the forward produced), and its rows of
+      // dWo = O_c^T dY.
+      UPIPE_LAUNCH(kAttnFwd, st,
+                   launch_attn_fwd(Qc, Kp, Vp, Oc, lse_r, S, Sp, S, Sp, 0, U, h0, G, 1, st));
+      UPIPE_LAUNCH(kRowdotLse, st,
+                   launch_rowdot_lse(dOc, HEAD_DIM, head, Oc, HEAD_DIM, head, lse_r, S, h0, U,
+                                     Sp, D, lse_c, st));
+      rc = wgrad(operand(Oc, HEAD_DIM, w, S, HEAD_DIM, head), dYn, w, dm,
+                 dwo + (int64_t)h0 * HEAD_DIM * dm, dm);
+      if (rc != UPIPE_OK) return rc;
+    } else {
+      UPIPE_LAUNCH(kRowdotLse, st,
+                   launch_rowdot_lse(dOc, HEAD_DIM, head, o_saved + (int64_t)h0 * HEAD_DIM, qw,
+                                     HEAD_DIM, lse, S, h0, U, Sp, D, lse_c, st));
+    }
     UPIPE_LAUNCH(kAttnBwdDkdv, st,
                  launch_attn_bwd_dkdv(Qc, dOc, lse_c, D, Kp, Vp, dK32, dV32, dKh, dVh, HEAD_DIM,
                                       head, S, Sp, U, h0, G, 1, st));
@@ -314,9 +338,13 @@ int upipe_layer_bwd(const void* x, const void* wqkv, const void* wo, const void*
     RopeArgs rope;
     rc = make_rope(rope_base, pos0, S, &rope);
     if (rc != UPIPE_OK) return rc;
-    if (!aligned16(x) || !aligned16(wqkv) || !aligned16(wo) || !aligned16(o_saved) ||
-        !aligned16(lse_saved) || !aligned16(dy) || !aligned16(dx) || !aligned16(dwqkv) ||
-        !aligned16(dwo) || !aligned16(ws))
+    // o_saved and lse_saved: both given (kept attention output), or both NULL
+    // (full checkpointing: recomputed).
+    if ((o_saved == nullptr) != (lse_saved == nullptr)) return UPIPE_ERR_INVALID_ARG;
+    const bool kept = o_saved != nullptr;
+    if (!aligned16(x) || !aligned16(wqkv) || !aligned16(wo) || (kept && !aligned16(o_saved)) ||
+        (kept && !aligned16(lse_saved)) || !aligned16(dy) || !aligned16(dx) ||
+        !aligned16(dwqkv) || !aligned16(dwo) || !aligned16(ws))
       return UPIPE_ERR_INVALID_ARG;
     if (ws_bytes < plan_layer_bwd(S, d_model, Hq, Hkv, U).total) return UPIPE_ERR_WORKSPACE;
     return run_layer_bwd((const bf16*)x, (const bf16*)wqkv, (const bf16*)wo,

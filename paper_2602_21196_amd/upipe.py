@@ -349,7 +349,9 @@ def layer_fwd(x, wqkv, wo, Hq, Hkv, d=128, U=1, ws=None, rope_base=0.0, pos0=0):
 
 def layer_bwd(x, wqkv, wo, o_saved, lse_saved, dy, Hq, Hkv, d=128, U=1,
               ws=None, rope_base=0.0, pos0=0):
-    """dx [S,dm], dwqkv [dm,(Hq+2Hkv)d], dwo [Hq d, dm], all bf16."""
+    """dx [S,dm], dwqkv [dm,(Hq+2Hkv)d], dwo [Hq d, dm], all bf16.
+    o_saved = lse_saved = None recomputes the attention output (full
+    checkpointing) instead of reading the kept one."""
     torch = _torch()
     S, dm = x.shape
     need = upipe_layer_bwd_workspace_size(S, dm, Hq, Hkv, d, U)
@@ -361,9 +363,13 @@ def layer_bwd(x, wqkv, wo, o_saved, lse_saved, dy, Hq, Hkv, d=128, U=1,
     dwqkv = torch.empty_like(wqkv)
     dwo = torch.empty_like(wo)
     bf = torch.bfloat16
+    kept = o_saved is not None
+    if kept != (lse_saved is not None):
+        raise ValueError("layer_bwd: pass both o_saved and lse_saved, or neither")
     st = upipe_layer_bwd(_ptr(x, bf, "x"), _ptr(wqkv, bf, "wqkv"),
-                         _ptr(wo, bf, "wo"), _ptr(o_saved, bf, "o_saved"),
-                         _ptr(lse_saved, torch.float32, "lse_saved"),
+                         _ptr(wo, bf, "wo"),
+                         _ptr(o_saved, bf, "o_saved") if kept else None,
+                         _ptr(lse_saved, torch.float32, "lse_saved") if kept else None,
                          _ptr(dy, bf, "dy"), _ptr(dx, bf, "dx"),
                          _ptr(dwqkv, bf, "dwqkv"), _ptr(dwo, bf, "dwo"),
                          S, dm, Hq, Hkv, d, U, float(rope_base), int(pos0),

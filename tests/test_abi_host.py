@@ -190,6 +190,20 @@ def test_layer_rope_arguments_validate(fn):
     assert _layer(fn, pos0=(1 << 32) - 255) == UNS
 
 
+def test_layer_bwd_saved_output_both_or_neither():
+    INV, WS = -1, -3
+    S, dm = 256, 512
+
+    def bwd(o, lse):
+        return upipe.upipe_layer_bwd(FAKE, FAKE, FAKE, o, lse, FAKE, FAKE, FAKE, FAKE, S, dm, 4,
+                                     1, 128, 1, 0.0, 0, FAKE, 0, None)
+    assert bwd(FAKE, FAKE) == WS           # kept output (selective checkpointing)
+    assert bwd(None, None) == WS           # recomputed (full checkpointing)
+    assert bwd(FAKE, None) == INV
+    assert bwd(None, FAKE) == INV
+    assert bwd(FAKE + 8, FAKE) == INV      # misaligned
+
+
 def test_rope_entry_point_validates():
     INV, UNS = -1, -2
     r = upipe.upipe_rope

@@ -130,3 +130,33 @@ def test_llama8b_layer_share_sampled():
     dqkv = np.concatenate([dq_t.reshape(len(tail), -1), dk_t.reshape(len(tail), -1),
                            dv_t.reshape(len(tail), -1)], axis=1)
     assert_close("dx tail rows", dx[j0:], dqkv @ w64.T)
+
+
+@pytest.mark.parametrize("S,dm,Hq,Hkv,base", [(300, 256, 4, 1, 0.0), (513, 384, 4, 2, 5e5),
+                                              (2048, 1024, 8, 2, 1e6)])
+def test_full_checkpointing_equals_kept_output(S, dm, Hq, Hkv, base):
+    """Backward without the saved attention output (each chunk's forward
+    recomputed) gives bitwise the results of the backward that reads it, for
+    every U; and both match the oracle."""
+    up = _upipe()
+    x, wqkv, wo, dy = W.layer_inputs(S, dm, Hq, Hkv, 128, 80 + S)
+    xd, wd, wod, dyd = (t.to(DEV) for t in (x, wqkv, wo, dy))
+    first = None
+    for U in [u for u in range(1, Hq + 1) if Hq % u == 0]:
+        print(f"full checkpointing S={S} dm={dm} Hq={Hq} Hkv={Hkv} U={U}", flush=True)
+        y, o, lse = up.layer_fwd(xd, wd, wod, Hq, Hkv, U=U, rope_base=base)
+        kept = up.layer_bwd(xd, wd, wod, o, lse, dyd, Hq, Hkv, U=U, rope_base=base)
+        full = up.layer_bwd(xd, wd, wod, None, None, dyd, Hq, Hkv, U=U, rope_base=base)
+        torch.cuda.synchronize()
+        for name, a, b in zip(("dx", "dwqkv", "dwo"), kept, full):
+            assert _bits_equal(a, b), f"{name}: kept vs recomputed output, U={U}"
+        if first is None:
+            first = [t.cpu() for t in full]
+        else:
+            for name, a, b in zip(("dx", "dwqkv", "dwo"), first, full):
+                assert _bits_equal(a, b.cpu()), f"{name}: U=1 vs U={U}"
+    x64, w64, wo64, dy64 = (as64(t) for t in (x, wqkv, wo, dy))
+    rb = base if base else None
+    ref = L.layer_bwd(x64, w64, wo64, dy64, Hq, Hkv, 128, rope_base=rb)
+    for name, g, r, bl in zip(("dx", "dwqkv", "dwo"), first, ref, (None, _blocks(Hq, Hkv)[4], None)):
+        assert_close(name, g, r, rms_scaled=name != "dx", blocks=bl)
