@@ -44,6 +44,9 @@ def parse():
     p.add_argument("--no-sweep", action="store_true",
                    help="skip the per-U throughput/memory sweep")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--batch", type=int, default=1,
+                   help="sequences per step (each of the workload's length S), run "
+                        "through one workspace")
     p.add_argument("--checkpointing", choices=("selective", "full"), default="selective",
                    help="layer workloads: keep the attention output for the backward "
                         "(selective) or recompute it there (full)")
@@ -174,14 +177,18 @@ def main():
     if w.extra.get("ring"):
         return ring_bench(args, w)
     dev = "cuda:0"
-    S, Hq, Hkv, d, U = w.S, w.Hq, w.Hkv, w.d, args.U
+    S, Hq, Hkv, d, U, B = w.S, w.Hq, w.Hkv, w.d, args.U, args.batch
     fwd_flops, bwd_flops = W.attention_flops(S, Hq, d)
-    step_flops = fwd_flops + bwd_flops
+    step_flops = B * (fwd_flops + bwd_flops)
     if w.is_layer:
         dm = w.d_model
-        x, wqkv, wo, dy = (t.to(dev) for t in W.inputs_for(w))
+        if B == 1:
+            x, wqkv, wo, dy = (t.to(dev) for t in W.inputs_for(w))
+        else:
+            x, wqkv, wo, dy = (t.to(dev) for t in
+                               W.batch_layer_inputs(S, dm, Hq, Hkv, d, w.seed, B))
         proj_fwd = 2 * S * dm * (Hq + 2 * Hkv) * d + 2 * S * Hq * d * dm
-        step_flops += 3 * proj_fwd
+        step_flops += 3 * proj_fwd * B
         ws_f = upipe.workspace(upipe.upipe_layer_fwd_workspace_size(S, dm, Hq, Hkv, d, U), dev)
         ws_b = upipe.workspace(upipe.upipe_layer_bwd_workspace_size(S, dm, Hq, Hkv, d, U), dev)
 
@@ -192,7 +199,7 @@ def main():
         # Tensors the forward leaves for the backward besides x and the
         # weights: the attention output and its lse under selective
         # checkpointing, nothing under full checkpointing.
-        kept_bytes = 0 if full_ac else 2 * S * Hq * d + 4 * Hq * S
+        kept_bytes = 0 if full_ac else B * (2 * S * Hq * d + 4 * Hq * S)
 
         def step():
             y, o, lse = upipe.layer_fwd(x, wqkv, wo, Hq, Hkv, d, U=U, ws=ws_f,
@@ -202,7 +209,10 @@ def main():
             upipe.layer_bwd(x, wqkv, wo, o, lse, dy, Hq, Hkv, d, U=U, ws=ws_b,
                             rope_base=rope_base)
     else:
-        q, k, v, do = W.attention_inputs(S, Hq, Hkv, d, w.seed)
+        if B == 1:
+            q, k, v, do = W.attention_inputs(S, Hq, Hkv, d, w.seed)
+        else:
+            q, k, v, do = W.batch_attention_inputs(S, Hq, Hkv, d, w.seed, B)
         qd, kd, vd, dod = (t.to(dev) for t in (q, k, v, do))
         ws_f = upipe.workspace(upipe.upipe_attn_fwd_workspace_size(S, Hq, Hkv, d, U), dev)
         ws_b = upipe.workspace(upipe.upipe_attn_bwd_workspace_size(S, Hq, Hkv, d, U), dev)
@@ -255,7 +265,7 @@ def main():
            "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
            "data": "synthetic",
            "config": {"workload": w.name, "S": S, "Hq": Hq, "Hkv": Hkv,
-                      "d": d, "U": U, "causal": True, "seed": w.seed,
+                      "d": d, "U": U, "causal": True, "seed": w.seed, "batch": B,
                       **({"d_model": w.d_model, "rope_base": rope_base,
                           "checkpointing": args.checkpointing} if w.is_layer else {})},
            "frac_of_peak": round(value / PEAK_BF16_TFLOPS, 4),
@@ -268,7 +278,7 @@ def main():
             "bwd_workspace": round(upipe.upipe_layer_bwd_workspace_size(S, w.d_model, Hq, Hkv,
                                                                          d, U) / 1e9, 4)}
 
-    if not args.no_sweep and not w.is_layer:
+    if not args.no_sweep and not w.is_layer and B == 1:
         del ws_f, ws_b
         torch.cuda.synchronize()
         # outputs of one fwd+bwd: o, dq [S,Hq,d] bf16, dk, dv [S,Hkv,d] bf16,
@@ -307,7 +317,7 @@ def main():
             "the group size, so the fit over all U is not exactly linear")
         out["tflops_vs_U"] = sweep_tf
 
-    if not args.no_cpu_baseline and not w.is_layer:
+    if not args.no_cpu_baseline and not w.is_layer and B == 1:
         out["cpu_baseline"] = cpu_baseline(w, q, k, v, do, args.cpu_seconds)
     print(json.dumps(out), flush=True)
 

@@ -95,6 +95,8 @@ int upipe_gqa_schedule(int H, int Hkv, int C, int U, int* stage_heads,
  * Workspace size queries.  Return the byte count the matching compute call
  * needs for these shapes, or 0 if the shapes are invalid or unsupported.
  * The size is  fixed(S, Hkv[, d_model]) + U * per_head(S)  (chunk buffers).
+ * It does not depend on the batch size B: the calls that take a batch of B
+ * sequences run them one after another through the same workspace.
  * ---------------------------------------------------------------------- */
 size_t upipe_attn_fwd_workspace_size(int64_t S, int Hq, int Hkv, int d, int U);
 size_t upipe_attn_bwd_workspace_size(int64_t S, int Hq, int Hkv, int d, int U);
@@ -105,20 +107,22 @@ size_t upipe_layer_bwd_workspace_size(int64_t S, int d_model, int Hq, int Hkv,
 
 /* ------------------------------------------------------------------------
  * Attention forward, head chunk by head chunk (Section 2.1 definition,
- * Section 3.3 chunking, Appendix A "Untied Ulysses (forward)").
+ * Section 3.3 chunking, Appendix A "Untied Ulysses (forward)"), for a batch
+ * of B independent sequences of length S (B >= 1; the paper's batch-size
+ * ablation spends the memory UPipe saves on B > 1).
  *
- *   q   bf16 [S, Hq, d]   queries, token-major (the Ulysses layout)
- *   k   bf16 [S, Hkv, d]  keys
- *   v   bf16 [S, Hkv, d]  values
- *   o   bf16 [S, Hq, d]   out: softmax(q k^T / sqrt d) v per head
- *   lse fp32 [Hq, S]      out: natural-log log-sum-exp of each row's scaled
- *                         scores (saved for the backward)
+ *   q   bf16 [B, S, Hq, d]   queries, token-major (the Ulysses layout)
+ *   k   bf16 [B, S, Hkv, d]  keys
+ *   v   bf16 [B, S, Hkv, d]  values
+ *   o   bf16 [B, S, Hq, d]   out: softmax(q k^T / sqrt d) v per head
+ *   lse fp32 [B, Hq, S]      out: natural-log log-sum-exp of each row's
+ *                            scaled scores (saved for the backward)
  * For each chunk c the U heads [cU, (c+1)U) are packed to a head-major chunk
  * buffer (the stand-in for the input all-to-all's destination), attended, and
  * unpacked into o (the output all-to-all's target, `final_out`).
  * ---------------------------------------------------------------------- */
 int upipe_attn_fwd(const void* q, const void* k, const void* v, void* o,
-                   float* lse, int64_t S, int Hq, int Hkv, int d, int causal,
+                   float* lse, int64_t B, int64_t S, int Hq, int Hkv, int d, int causal,
                    int U, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
@@ -166,17 +170,17 @@ int upipe_lse_merge(void* o, float* lse, const void* o_part, const float* lse_pa
  * Appendix A "Untied Ulysses (backward)": per-stage dQ, per-group dK/dV
  * accumulators that persist across stages).
  *
- *   q, k, v, o, lse  as produced/consumed by upipe_attn_fwd
- *   dout bf16 [S, Hq, d]   upstream gradient of o
- *   dq   bf16 [S, Hq, d]   out
- *   dk   bf16 [S, Hkv, d]  out: summed over each group's query heads
- *   dv   bf16 [S, Hkv, d]  out
+ *   q, k, v, o, lse  as produced/consumed by upipe_attn_fwd (same B, S)
+ *   dout bf16 [B, S, Hq, d]   upstream gradient of o
+ *   dq   bf16 [B, S, Hq, d]   out
+ *   dk   bf16 [B, S, Hkv, d]  out: summed over each group's query heads
+ *   dv   bf16 [B, S, Hkv, d]  out
  * `lse` must come from upipe_attn_fwd on the same q, k, v (it is used to
  * rebuild the probabilities without a second softmax pass).
  * ---------------------------------------------------------------------- */
 int upipe_attn_bwd(const void* q, const void* k, const void* v, const void* o,
                    const float* lse, const void* dout, void* dq, void* dk,
-                   void* dv, int64_t S, int Hq, int Hkv, int d, int causal,
+                   void* dv, int64_t B, int64_t S, int Hq, int Hkv, int d, int causal,
                    int U, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
@@ -200,15 +204,16 @@ int upipe_rope(void* x, int64_t S, int H, int d, int64_t pos0, double base, int 
  * Attention block forward (Section 3.3, Appendix A "Untied Ulysses
  * (forward)": per stage, QKV projection of the stage's heads, attention,
  * output written into its slot of `final_out`; after the last stage the
- * output projection y = final_out wo).  Always causal.
+ * output projection y = final_out wo).  Always causal.  A batch of B >= 1
+ * independent sequences of length S; every sequence starts at position pos0.
  *
- *   x         bf16 [S, d_model]                  hidden states
+ *   x         bf16 [B, S, d_model]               hidden states
  *   wqkv      bf16 [d_model, (Hq + 2 Hkv) d]     columns [Q heads|K|V]
  *   wo        bf16 [Hq d, d_model]               output projection
- *   y         bf16 [S, d_model]                  out: final_out @ wo
- *   o_saved   bf16 [S, Hq, d]                    out: final_out (attention
+ *   y         bf16 [B, S, d_model]               out: final_out @ wo
+ *   o_saved   bf16 [B, S, Hq, d]                 out: final_out (attention
  *                                                output, saved for backward)
- *   lse_saved fp32 [Hq, S]                       out: row log-sum-exp
+ *   lse_saved fp32 [B, Hq, S]                    out: row log-sum-exp
  *   rope_base  0: no rotary embedding; > 0: Q and K heads are rotated as by
  *              upipe_rope(base = rope_base, pos0) inside the projection,
  *              before their single rounding to bf16 (Section 4
@@ -217,7 +222,7 @@ int upipe_rope(void* x, int64_t S, int H, int d, int64_t pos0, double base, int 
  * d_model must be a multiple of 128.
  * ---------------------------------------------------------------------- */
 int upipe_layer_fwd(const void* x, const void* wqkv, const void* wo, void* y,
-                    void* o_saved, float* lse_saved, int64_t S, int d_model,
+                    void* o_saved, float* lse_saved, int64_t B, int64_t S, int d_model,
                     int Hq, int Hkv, int d, int U, double rope_base, int64_t pos0,
                     void* ws, size_t ws_bytes, hipStream_t stream);
 
@@ -230,7 +235,7 @@ int upipe_layer_fwd(const void* x, const void* wqkv, const void* wo, void* y,
  * one product.  K and V are recomputed from x (activation checkpointing
  * keeps only x, final_out, lse).
  *
- *   x, wqkv, wo        as for upipe_layer_fwd
+ *   x, wqkv, wo, B     as for upipe_layer_fwd
  *   rope_base, pos0    as for upipe_layer_fwd (the same values): Q and K are
  *                      recomputed rotated, and the gradients of the rotated
  *                      Q and K are turned back by the inverse rotation
@@ -241,17 +246,18 @@ int upipe_layer_fwd(const void* x, const void* wqkv, const void* wo, void* y,
  *                      chunk's attention forward is recomputed, bitwise
  *                      equal to the forward's, at the cost of one more
  *                      attention forward; the results are identical)
- *   dy    bf16 [S, d_model]                 upstream gradient of y
- *   dx    bf16 [S, d_model]                 out
- *   dwqkv bf16 [d_model, (Hq + 2 Hkv) d]    out
- *   dwo   bf16 [Hq d, d_model]              out
+ *   dy    bf16 [B, S, d_model]              upstream gradient of y
+ *   dx    bf16 [B, S, d_model]              out
+ *   dwqkv bf16 [d_model, (Hq + 2 Hkv) d]    out: summed over the batch
+ *   dwo   bf16 [Hq d, d_model]              out: summed over the batch
  * Weight gradients reduce over S with a fixed split of the sequence and a
- * fixed-order sum of the partial products (deterministic, no atomics).
+ * fixed-order sum of the partial products, then over the batch in sequence
+ * order in fp32, rounded once (deterministic, no atomics).
  * ---------------------------------------------------------------------- */
 int upipe_layer_bwd(const void* x, const void* wqkv, const void* wo,
                     const void* o_saved, const float* lse_saved,
                     const void* dy, void* dx, void* dwqkv, void* dwo,
-                    int64_t S, int d_model, int Hq, int Hkv, int d, int U,
+                    int64_t B, int64_t S, int d_model, int Hq, int Hkv, int d, int U,
                     double rope_base, int64_t pos0, void* ws, size_t ws_bytes,
                     hipStream_t stream);
 

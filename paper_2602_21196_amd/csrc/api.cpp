@@ -269,9 +269,10 @@ size_t upipe_attn_bwd_workspace_size(int64_t S, int Hq, int Hkv, int d, int U) {
 }
 
 int upipe_attn_fwd(const void* q, const void* k, const void* v, void* o,
-                   float* lse, int64_t S, int Hq, int Hkv, int d, int causal,
+                   float* lse, int64_t B, int64_t S, int Hq, int Hkv, int d, int causal,
                    int U, void* ws, size_t ws_bytes, hipStream_t stream) {
   try {
+    if (B < 1) return UPIPE_ERR_INVALID_ARG;
     int rc = check_attn_shape(S, Hq, Hkv, d, U);
     if (rc != UPIPE_OK) return rc;
     if (causal != 0 && causal != 1) return UPIPE_ERR_INVALID_ARG;
@@ -279,8 +280,15 @@ int upipe_attn_fwd(const void* q, const void* k, const void* v, void* o,
         !aligned16(lse) || !aligned16(ws))
       return UPIPE_ERR_INVALID_ARG;
     if (ws_bytes < plan_attn_fwd(S, Hq, Hkv, U).total) return UPIPE_ERR_WORKSPACE;
-    return run_attn_fwd((const bf16*)q, (const bf16*)k, (const bf16*)v, (bf16*)o, lse, S,
-                        Hq, Hkv, causal, U, (char*)ws, stream);
+    // The B sequences run one after another through the same workspace.
+    const int64_t qs = S * Hq * HEAD_DIM, ks = S * Hkv * HEAD_DIM, ls = (int64_t)Hq * S;
+    for (int64_t b = 0; b < B; ++b) {
+      rc = run_attn_fwd((const bf16*)q + b * qs, (const bf16*)k + b * ks,
+                        (const bf16*)v + b * ks, (bf16*)o + b * qs, lse + b * ls, S, Hq, Hkv,
+                        causal, U, (char*)ws, stream);
+      if (rc != UPIPE_OK) return rc;
+    }
+    return UPIPE_OK;
   } catch (...) {
     return UPIPE_ERR_HIP;
   }
@@ -354,9 +362,10 @@ int upipe_rope(void* x, int64_t S, int H, int d, int64_t pos0, double base, int 
 
 int upipe_attn_bwd(const void* q, const void* k, const void* v, const void* o,
                    const float* lse, const void* dout, void* dq, void* dk,
-                   void* dv, int64_t S, int Hq, int Hkv, int d, int causal,
+                   void* dv, int64_t B, int64_t S, int Hq, int Hkv, int d, int causal,
                    int U, void* ws, size_t ws_bytes, hipStream_t stream) {
   try {
+    if (B < 1) return UPIPE_ERR_INVALID_ARG;
     int rc = check_attn_shape(S, Hq, Hkv, d, U);
     if (rc != UPIPE_OK) return rc;
     if (causal != 0 && causal != 1) return UPIPE_ERR_INVALID_ARG;
@@ -365,9 +374,15 @@ int upipe_attn_bwd(const void* q, const void* k, const void* v, const void* o,
         !aligned16(dv) || !aligned16(ws))
       return UPIPE_ERR_INVALID_ARG;
     if (ws_bytes < plan_attn_bwd(S, Hq, Hkv, U).total) return UPIPE_ERR_WORKSPACE;
-    return run_attn_bwd((const bf16*)q, (const bf16*)k, (const bf16*)v, (const bf16*)o, lse,
-                        (const bf16*)dout, (bf16*)dq, (bf16*)dk, (bf16*)dv, S, Hq, Hkv,
-                        causal, U, (char*)ws, stream);
+    const int64_t qs = S * Hq * HEAD_DIM, ks = S * Hkv * HEAD_DIM, ls = (int64_t)Hq * S;
+    for (int64_t b = 0; b < B; ++b) {
+      rc = run_attn_bwd((const bf16*)q + b * qs, (const bf16*)k + b * ks,
+                        (const bf16*)v + b * ks, (const bf16*)o + b * qs, lse + b * ls,
+                        (const bf16*)dout + b * qs, (bf16*)dq + b * qs, (bf16*)dk + b * ks,
+                        (bf16*)dv + b * ks, S, Hq, Hkv, causal, U, (char*)ws, stream);
+      if (rc != UPIPE_OK) return rc;
+    }
+    return UPIPE_OK;
   } catch (...) {
     return UPIPE_ERR_HIP;
   }

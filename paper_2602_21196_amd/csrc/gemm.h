@@ -70,8 +70,11 @@ hipError_t launch_gemm(const GemmOperand& A, bool a_kmajor, const GemmOperand& B
                        const GemmEpilogue& E, int epi, int64_t M, int64_t N, int64_t k_begin,
                        int64_t k_len, int splits, hipStream_t st);
 
-// out[m * ldo + col0 + n] = bf16(sum_s partial[s][m][n]) in ascending s.
+// t = sum_s partial[s][m][n] in ascending s, plus acc32[m][n] unless first;
+// t goes to acc32[m][n] unless last, else out[m * ldo + col0 + n] = bf16(t).
+// (first = last = 1 never touches acc32.)
 hipError_t launch_reduce_splitk(const float* partial, int splits, int64_t M, int64_t N, bf16* out,
-                                int64_t ldo, int64_t col0, hipStream_t st);
+                                int64_t ldo, int64_t col0, float* acc32, int first, int last,
+                                hipStream_t st);
 
 }  // namespace upipe

@@ -231,18 +231,25 @@ __global__ __launch_bounds__(256, 3 - GemmStages<EPI>::N) void gemm_kernel(
     }
 }
 
-// out[m * ldo + col0 + n] = bf16(sum over splits s = 0.. of partial[s][m][n]),
-// summed in ascending s.
+// t = sum over splits s = 0.. of partial[s][m][n], summed in ascending s,
+// then added to acc32[m][n] unless `first`; the total goes to acc32 unless
+// `last`, else to out[m * ldo + col0 + n] as bf16.
 __global__ __launch_bounds__(256) void reduce_splitk_kernel(const float* __restrict__ partial,
                                                             int splits, int64_t M, int64_t N,
                                                             bf16* __restrict__ out, int64_t ldo,
-                                                            int64_t col0) {
+                                                            int64_t col0, float* __restrict__ acc32,
+                                                            int first, int last) {
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (idx >= M * N) return;
   float s = 0.f;
   for (int k = 0; k < splits; ++k) s += partial[(int64_t)k * M * N + idx];
-  const int64_t m = idx / N, n = idx % N;
-  out[m * ldo + col0 + n] = (bf16)s;
+  if (!first) s = acc32[idx] + s;
+  if (last) {
+    const int64_t m = idx / N, n = idx % N;
+    out[m * ldo + col0 + n] = (bf16)s;
+  } else {
+    acc32[idx] = s;
+  }
 }
 
 template <bool A_K, bool B_K, int EPI>
@@ -277,10 +284,11 @@ hipError_t launch_gemm(const GemmOperand& A, bool a_kmajor, const GemmOperand& B
 }
 
 hipError_t launch_reduce_splitk(const float* partial, int splits, int64_t M, int64_t N, bf16* out,
-                                int64_t ldo, int64_t col0, hipStream_t st) {
+                                int64_t ldo, int64_t col0, float* acc32, int first, int last,
+                                hipStream_t st) {
   const int64_t n = M * N;
   hipLaunchKernelGGL(reduce_splitk_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
-                     partial, splits, M, N, out, ldo, col0);
+                     partial, splits, M, N, out, ldo, col0, acc32, first, last);
   return hipGetLastError();
 }
 

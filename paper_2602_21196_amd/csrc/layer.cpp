@@ -75,7 +75,9 @@ struct LayerBwdPlan {
   bool carry = false;          // a key/value group spans several chunks
   size_t Kp = 0, Vp = 0, dK32 = 0, dV32 = 0, Qc = 0, D = 0, lse_c = 0;
   size_t Oc = 0, lse_r = 0;    // recomputed attention output (full checkpointing)
-  size_t dFO = 0, dQKV = 0, partial = 0, total = 0;
+  size_t dFO = 0, dQKV = 0, partial = 0;
+  size_t dWqkv32 = 0, dWo32 = 0;   // weight-gradient sums over a batch of sequences
+  size_t total = 0;
 };
 
 LayerFwdPlan plan_layer_fwd(int64_t S, int d_model, int Hq, int Hkv, int U) {
@@ -119,6 +121,8 @@ LayerBwdPlan plan_layer_bwd(int64_t S, int d_model, int Hq, int Hkv, int U) {
   // 2Hkv) d] or dWo [Hq d, d_model].
   const int64_t widest = (int64_t)(Hq + 2 * Hkv) * HEAD_DIM;
   p.partial = c.take((size_t)p.splits * d_model * widest * 4);
+  p.dWqkv32 = c.take((size_t)d_model * widest * 4);
+  p.dWo32 = c.take((size_t)Hq * HEAD_DIM * d_model * 4);
   p.total = c.used;
   return p;
 }
@@ -156,9 +160,10 @@ hipError_t gemm1(const GemmOperand& A, bool ak, const GemmOperand& B, bool bk, G
 
 }  // namespace
 
-int run_layer_fwd(const bf16* x, const bf16* wqkv, const bf16* wo, bf16* y, bf16* o_saved,
-                  float* lse, int64_t S, int dm, int Hq, int Hkv, int U, RopeArgs rope,
-                  char* ws, hipStream_t st) {
+// One sequence of the batch.
+int run_layer_fwd_seq(const bf16* x, const bf16* wqkv, const bf16* wo, bf16* y, bf16* o_saved,
+                      float* lse, int64_t S, int dm, int Hq, int Hkv, int U, RopeArgs rope,
+                      char* ws, hipStream_t st) {
   const LayerFwdPlan p = plan_layer_fwd(S, dm, Hq, Hkv, U);
   const int64_t Sp = p.Sp, ldw = (int64_t)(Hq + 2 * Hkv) * HEAD_DIM;
   const int64_t qw = (int64_t)Hq * HEAD_DIM;
@@ -188,9 +193,13 @@ int run_layer_fwd(const bf16* x, const bf16* wqkv, const bf16* wo, bf16* y, bf16
   return UPIPE_OK;
 }
 
-int run_layer_bwd(const bf16* x, const bf16* wqkv, const bf16* wo, const bf16* o_saved,
-                  const float* lse, const bf16* dy, bf16* dx, bf16* dwqkv, bf16* dwo, int64_t S,
-                  int dm, int Hq, int Hkv, int U, RopeArgs rope, char* ws, hipStream_t st) {
+// One sequence of the batch: dx of the sequence; the weight gradients of
+// the sequence are added to the fp32 sums unless `first` and rounded into
+// dwqkv, dwo when `last`.
+int run_layer_bwd_seq(const bf16* x, const bf16* wqkv, const bf16* wo, const bf16* o_saved,
+                      const float* lse, const bf16* dy, bf16* dx, bf16* dwqkv, bf16* dwo,
+                      int64_t S, int dm, int Hq, int Hkv, int U, RopeArgs rope, int first,
+                      int last, char* ws, hipStream_t st) {
   const LayerBwdPlan p = plan_layer_bwd(S, dm, Hq, Hkv, U);
   const int64_t Sp = p.Sp, ldw = (int64_t)(Hq + 2 * Hkv) * HEAD_DIM;
   const int64_t qw = (int64_t)Hq * HEAD_DIM, kvw = (int64_t)Hkv * HEAD_DIM;
@@ -210,6 +219,8 @@ int run_layer_bwd(const bf16* x, const bf16* wqkv, const bf16* wo, const bf16* o
   bf16* dKh = dQKV + (int64_t)Hq * head;
   bf16* dVh = dKh + (int64_t)Hkv * head;
   float* partial = (float*)(ws + p.partial);
+  float* dWqkv32 = (float*)(ws + p.dWqkv32);
+  float* dWo32 = (float*)(ws + p.dWo32);
   const int G = Hq / Hkv;
   const int64_t nqkv = (int64_t)(Hq + 2 * Hkv) * HEAD_DIM;
   const GemmOperand X = operand(x, dm, S, dm);
@@ -218,9 +229,10 @@ int run_layer_bwd(const bf16* x, const bf16* wqkv, const bf16* wo, const bf16* o
   const GemmOperand dYn = operand(dy, dm, dm, S);      // MN-major view: (n = col, k = s)
 
   // Weight gradient C[M][N] = sum over s of A(m, s) B(n, s), split into fixed
-  // pieces of the sequence and summed in order into out[m * ldo + n].
+  // pieces of the sequence and summed in order (then onto the batch sum
+  // acc32 [M][N]) into out[m * ldo + n].
   auto wgrad = [&](const GemmOperand& A, const GemmOperand& B, int64_t M, int64_t N, bf16* out,
-                   int64_t ldo) -> int {
+                   int64_t ldo, float* acc32) -> int {
     GemmEpilogue e{};
     e.partial = partial;
     e.k_total = S;
@@ -228,7 +240,8 @@ int run_layer_bwd(const bf16* x, const bf16* wqkv, const bf16* wo, const bf16* o
                  launch_gemm(A, false, B, false, e, GEMM_EPI_PARTIAL, M, N, 0, p.split_len,
                              p.splits, st));
     UPIPE_LAUNCH(kReduceSplitk, st,
-                 launch_reduce_splitk(partial, p.splits, M, N, out, ldo, 0, st));
+                 launch_reduce_splitk(partial, p.splits, M, N, out, ldo, 0, acc32, first, last,
+                                      st));
     return UPIPE_OK;
   };
 
@@ -242,7 +255,7 @@ int run_layer_bwd(const bf16* x, const bf16* wqkv, const bf16* wo, const bf16* o
                      GEMM_EPI_HEADS, Sp, qw, dm, st));
   int rc;
   if (!recompute) {   // dWo = final_out^T dY from the kept final_out
-    rc = wgrad(operand(o_saved, qw, qw, S), dYn, qw, dm, dwo, dm);
+    rc = wgrad(operand(o_saved, qw, qw, S), dYn, qw, dm, dwo, dm, dWo32);
     if (rc != UPIPE_OK) return rc;
   }
   for (int h0 = 0; h0 < Hq; h0 += U) {
@@ -263,7 +276,7 @@ int run_layer_bwd(const bf16* x, const bf16* wqkv, const bf16* wo, const bf16* o
                    launch_rowdot_lse(dOc, HEAD_DIM, head, Oc, HEAD_DIM, head, lse_r, S, h0, U,
                                      Sp, D, lse_c, st));
       rc = wgrad(operand(Oc, HEAD_DIM, w, S, HEAD_DIM, head), dYn, w, dm,
-                 dwo + (int64_t)h0 * HEAD_DIM * dm, dm);
+                 dwo + (int64_t)h0 * HEAD_DIM * dm, dm, dWo32 + (int64_t)h0 * HEAD_DIM * dm);
       if (rc != UPIPE_OK) return rc;
     } else {
       UPIPE_LAUNCH(kRowdotLse, st,
@@ -287,7 +300,38 @@ int run_layer_bwd(const bf16* x, const bf16* wqkv, const bf16* wo, const bf16* o
                      operand(wqkv, ldw, dm, nqkv), true, store_epi(dx, dm, S), GEMM_EPI_ACC32,
                      Sp, dm, nqkv, st));
   // dWqkv = x^T [dQ | dK | dV].
-  return wgrad(XT, operand(dQKV, HEAD_DIM, nqkv, S, HEAD_DIM, head), dm, nqkv, dwqkv, ldw);
+  return wgrad(XT, operand(dQKV, HEAD_DIM, nqkv, S, HEAD_DIM, head), dm, nqkv, dwqkv, ldw,
+               dWqkv32);
+}
+
+// Batches: the B sequences run one after another through the same
+// workspace; only the caller's tensors grow with B.
+int run_layer_fwd(const bf16* x, const bf16* wqkv, const bf16* wo, bf16* y, bf16* o_saved,
+                  float* lse, int64_t B, int64_t S, int dm, int Hq, int Hkv, int U, RopeArgs rope,
+                  char* ws, hipStream_t st) {
+  const int64_t xs = S * dm, os = S * Hq * HEAD_DIM, ls = (int64_t)Hq * S;
+  for (int64_t b = 0; b < B; ++b) {
+    const int rc = run_layer_fwd_seq(x + b * xs, wqkv, wo, y + b * xs, o_saved + b * os,
+                                     lse + b * ls, S, dm, Hq, Hkv, U, rope, ws, st);
+    if (rc != UPIPE_OK) return rc;
+  }
+  return UPIPE_OK;
+}
+
+int run_layer_bwd(const bf16* x, const bf16* wqkv, const bf16* wo, const bf16* o_saved,
+                  const float* lse, const bf16* dy, bf16* dx, bf16* dwqkv, bf16* dwo, int64_t B,
+                  int64_t S, int dm, int Hq, int Hkv, int U, RopeArgs rope, char* ws,
+                  hipStream_t st) {
+  const int64_t xs = S * dm, os = S * Hq * HEAD_DIM, ls = (int64_t)Hq * S;
+  const bool kept = o_saved != nullptr;
+  for (int64_t b = 0; b < B; ++b) {
+    const int rc = run_layer_bwd_seq(x + b * xs, wqkv, wo, kept ? o_saved + b * os : nullptr,
+                                     kept ? lse + b * ls : nullptr, dy + b * xs, dx + b * xs,
+                                     dwqkv, dwo, S, dm, Hq, Hkv, U, rope, b == 0, b == B - 1, ws,
+                                     st);
+    if (rc != UPIPE_OK) return rc;
+  }
+  return UPIPE_OK;
 }
 
 }  // namespace upipe
@@ -307,10 +351,11 @@ size_t upipe_layer_bwd_workspace_size(int64_t S, int d_model, int Hq, int Hkv, i
 }
 
 int upipe_layer_fwd(const void* x, const void* wqkv, const void* wo, void* y, void* o_saved,
-                    float* lse_saved, int64_t S, int d_model, int Hq, int Hkv, int d, int U,
-                    double rope_base, int64_t pos0, void* ws, size_t ws_bytes,
+                    float* lse_saved, int64_t B, int64_t S, int d_model, int Hq, int Hkv, int d,
+                    int U, double rope_base, int64_t pos0, void* ws, size_t ws_bytes,
                     hipStream_t stream) {
   try {
+    if (B < 1) return UPIPE_ERR_INVALID_ARG;
     int rc = check_layer_shape(S, d_model, Hq, Hkv, d, U);
     if (rc != UPIPE_OK) return rc;
     RopeArgs rope;
@@ -321,7 +366,7 @@ int upipe_layer_fwd(const void* x, const void* wqkv, const void* wo, void* y, vo
       return UPIPE_ERR_INVALID_ARG;
     if (ws_bytes < plan_layer_fwd(S, d_model, Hq, Hkv, U).total) return UPIPE_ERR_WORKSPACE;
     return run_layer_fwd((const bf16*)x, (const bf16*)wqkv, (const bf16*)wo, (bf16*)y,
-                         (bf16*)o_saved, lse_saved, S, d_model, Hq, Hkv, U, rope, (char*)ws,
+                         (bf16*)o_saved, lse_saved, B, S, d_model, Hq, Hkv, U, rope, (char*)ws,
                          stream);
   } catch (...) {
     return UPIPE_ERR_HIP;
@@ -330,9 +375,11 @@ int upipe_layer_fwd(const void* x, const void* wqkv, const void* wo, void* y, vo
 
 int upipe_layer_bwd(const void* x, const void* wqkv, const void* wo, const void* o_saved,
                     const float* lse_saved, const void* dy, void* dx, void* dwqkv, void* dwo,
-                    int64_t S, int d_model, int Hq, int Hkv, int d, int U, double rope_base,
-                    int64_t pos0, void* ws, size_t ws_bytes, hipStream_t stream) {
+                    int64_t B, int64_t S, int d_model, int Hq, int Hkv, int d, int U,
+                    double rope_base, int64_t pos0, void* ws, size_t ws_bytes,
+                    hipStream_t stream) {
   try {
+    if (B < 1) return UPIPE_ERR_INVALID_ARG;
     int rc = check_layer_shape(S, d_model, Hq, Hkv, d, U);
     if (rc != UPIPE_OK) return rc;
     RopeArgs rope;
@@ -349,7 +396,7 @@ int upipe_layer_bwd(const void* x, const void* wqkv, const void* wo, const void*
     if (ws_bytes < plan_layer_bwd(S, d_model, Hq, Hkv, U).total) return UPIPE_ERR_WORKSPACE;
     return run_layer_bwd((const bf16*)x, (const bf16*)wqkv, (const bf16*)wo,
                          (const bf16*)o_saved, lse_saved, (const bf16*)dy, (bf16*)dx,
-                         (bf16*)dwqkv, (bf16*)dwo, S, d_model, Hq, Hkv, U, rope, (char*)ws,
+                         (bf16*)dwqkv, (bf16*)dwo, B, S, d_model, Hq, Hkv, U, rope, (char*)ws,
                          stream);
   } catch (...) {
     return UPIPE_ERR_HIP;

@@ -37,11 +37,11 @@ _SIGNATURES = {
     "upipe_layer_fwd_workspace_size": (_size, [_i64, _int, _int, _int, _int, _int]),
     "upipe_layer_bwd_workspace_size": (_size, [_i64, _int, _int, _int, _int, _int]),
     "upipe_attn_fwd": (_int, [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _fptr,
-                              _i64, _int, _int, _int, _int, _int,
+                              _i64, _i64, _int, _int, _int, _int, _int,
                               _c_void_p, _size, _c_void_p]),
     "upipe_attn_bwd": (_int, [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _fptr,
                               _c_void_p, _c_void_p, _c_void_p, _c_void_p,
-                              _i64, _int, _int, _int, _int, _int,
+                              _i64, _i64, _int, _int, _int, _int, _int,
                               _c_void_p, _size, _c_void_p]),
     "upipe_attn_fwd_ring_workspace_size": (_size, [_i64, _i64, _int, _int, _int, _int]),
     "upipe_attn_fwd_ring": (_int, [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _fptr,
@@ -51,11 +51,11 @@ _SIGNATURES = {
                                _c_void_p]),
     "upipe_rope": (_int, [_c_void_p, _i64, _int, _int, _i64, _dbl, _int, _c_void_p]),
     "upipe_layer_fwd": (_int, [_c_void_p, _c_void_p, _c_void_p, _c_void_p,
-                               _c_void_p, _fptr, _i64, _int, _int, _int, _int,
+                               _c_void_p, _fptr, _i64, _i64, _int, _int, _int, _int,
                                _int, _dbl, _i64, _c_void_p, _size, _c_void_p]),
     "upipe_layer_bwd": (_int, [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _fptr,
                                _c_void_p, _c_void_p, _c_void_p, _c_void_p,
-                               _i64, _int, _int, _int, _int, _int, _dbl, _i64,
+                               _i64, _i64, _int, _int, _int, _int, _int, _dbl, _i64,
                                _c_void_p, _size, _c_void_p]),
     "upipe_profile_enable": (_int, [_int]),
     "upipe_profile_reset": (_int, []),
@@ -129,15 +129,15 @@ def upipe_layer_bwd_workspace_size(S, d_model, Hq, Hkv, d, U):
     return lib().upipe_layer_bwd_workspace_size(S, d_model, Hq, Hkv, d, U)
 
 
-def upipe_attn_fwd(q, k, v, o, lse, S, Hq, Hkv, d, causal, U, ws, ws_bytes,
+def upipe_attn_fwd(q, k, v, o, lse, B, S, Hq, Hkv, d, causal, U, ws, ws_bytes,
                    stream):
-    return lib().upipe_attn_fwd(q, k, v, o, lse, S, Hq, Hkv, d, causal, U, ws,
+    return lib().upipe_attn_fwd(q, k, v, o, lse, B, S, Hq, Hkv, d, causal, U, ws,
                                 ws_bytes, stream)
 
 
-def upipe_attn_bwd(q, k, v, o, lse, dout, dq, dk, dv, S, Hq, Hkv, d, causal,
+def upipe_attn_bwd(q, k, v, o, lse, dout, dq, dk, dv, B, S, Hq, Hkv, d, causal,
                    U, ws, ws_bytes, stream):
-    return lib().upipe_attn_bwd(q, k, v, o, lse, dout, dq, dk, dv, S, Hq, Hkv,
+    return lib().upipe_attn_bwd(q, k, v, o, lse, dout, dq, dk, dv, B, S, Hq, Hkv,
                                 d, causal, U, ws, ws_bytes, stream)
 
 
@@ -160,18 +160,18 @@ def upipe_rope(x, S, H, d, pos0, base, inverse, stream):
     return lib().upipe_rope(x, S, H, d, pos0, base, inverse, stream)
 
 
-def upipe_layer_fwd(x, wqkv, wo, y, o_saved, lse_saved, S, d_model, Hq, Hkv,
+def upipe_layer_fwd(x, wqkv, wo, y, o_saved, lse_saved, B, S, d_model, Hq, Hkv,
                     d, U, rope_base, pos0, ws, ws_bytes, stream):
-    return lib().upipe_layer_fwd(x, wqkv, wo, y, o_saved, lse_saved, S,
+    return lib().upipe_layer_fwd(x, wqkv, wo, y, o_saved, lse_saved, B, S,
                                  d_model, Hq, Hkv, d, U, rope_base, pos0, ws,
                                  ws_bytes, stream)
 
 
-def upipe_layer_bwd(x, wqkv, wo, o_saved, lse_saved, dy, dx, dwqkv, dwo, S,
+def upipe_layer_bwd(x, wqkv, wo, o_saved, lse_saved, dy, dx, dwqkv, dwo, B, S,
                     d_model, Hq, Hkv, d, U, rope_base, pos0, ws, ws_bytes,
                     stream):
     return lib().upipe_layer_bwd(x, wqkv, wo, o_saved, lse_saved, dy, dx,
-                                 dwqkv, dwo, S, d_model, Hq, Hkv, d, U,
+                                 dwqkv, dwo, B, S, d_model, Hq, Hkv, d, U,
                                  rope_base, pos0, ws, ws_bytes, stream)
 
 
@@ -231,22 +231,36 @@ def workspace(nbytes, device):
     return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
 
 
+def _batch(t, rank):
+    """(B, shape without the batch) of a tensor with an optional leading batch."""
+    if t.dim() == rank:
+        return 1, tuple(t.shape)
+    if t.dim() == rank + 1:
+        return t.shape[0], tuple(t.shape[1:])
+    raise ValueError(f"expected {rank} or {rank + 1} dimensions, got {t.dim()}")
+
+
+def _lse_shape(q, B, Hq, S):
+    return (Hq, S) if q.dim() == 3 else (B, Hq, S)
+
+
 def attn_fwd(q, k, v, causal=True, U=1, ws=None):
-    """o [S,Hq,d] bf16, lse [Hq,S] fp32 for q [S,Hq,d], k/v [S,Hkv,d] bf16."""
+    """o [(B,)S,Hq,d] bf16, lse [(B,)Hq,S] fp32 for q [(B,)S,Hq,d],
+    k/v [(B,)S,Hkv,d] bf16."""
     torch = _torch()
-    S, Hq, d = q.shape
-    Hkv = k.shape[1]
+    B, (S, Hq, d) = _batch(q, 3)
+    Hkv = k.shape[-2]
     need = upipe_attn_fwd_workspace_size(S, Hq, Hkv, d, U)
     if need == 0:
         raise UpipeError("upipe_attn_fwd_workspace_size", -1)
     if ws is None:
         ws = workspace(need, q.device)
     o = torch.empty_like(q)
-    lse = torch.empty((Hq, S), dtype=torch.float32, device=q.device)
+    lse = torch.empty(_lse_shape(q, B, Hq, S), dtype=torch.float32, device=q.device)
     bf = torch.bfloat16
     st = upipe_attn_fwd(_ptr(q, bf, "q"), _ptr(k, bf, "k"), _ptr(v, bf, "v"),
                         _ptr(o, bf, "o"), _ptr(lse, torch.float32, "lse"),
-                        S, Hq, Hkv, d, int(causal), U, ws.data_ptr(),
+                        B, S, Hq, Hkv, d, int(causal), U, ws.data_ptr(),
                         ws.numel(), _stream())
     _check("upipe_attn_fwd", st)
     return o, lse
@@ -290,10 +304,10 @@ def lse_merge(o, lse, o_part, lse_part):
 
 
 def attn_bwd(q, k, v, o, lse, dout, causal=True, U=1, ws=None):
-    """dq [S,Hq,d], dk, dv [S,Hkv,d] bf16."""
+    """dq [(B,)S,Hq,d], dk, dv [(B,)S,Hkv,d] bf16."""
     torch = _torch()
-    S, Hq, d = q.shape
-    Hkv = k.shape[1]
+    B, (S, Hq, d) = _batch(q, 3)
+    Hkv = k.shape[-2]
     need = upipe_attn_bwd_workspace_size(S, Hq, Hkv, d, U)
     if need == 0:
         raise UpipeError("upipe_attn_bwd_workspace_size", -1)
@@ -307,7 +321,7 @@ def attn_bwd(q, k, v, o, lse, dout, causal=True, U=1, ws=None):
                         _ptr(o, bf, "o"), _ptr(lse, torch.float32, "lse"),
                         _ptr(dout, bf, "dout"), _ptr(dq, bf, "dq"),
                         _ptr(dk, bf, "dk"), _ptr(dv, bf, "dv"),
-                        S, Hq, Hkv, d, int(causal), U, ws.data_ptr(),
+                        B, S, Hq, Hkv, d, int(causal), U, ws.data_ptr(),
                         ws.numel(), _stream())
     _check("upipe_attn_bwd", st)
     return dq, dk, dv
@@ -324,24 +338,25 @@ def rope(x, base, pos0=0, inverse=False):
 
 
 def layer_fwd(x, wqkv, wo, Hq, Hkv, d=128, U=1, ws=None, rope_base=0.0, pos0=0):
-    """y [S,dm] bf16, o_saved [S,Hq,d] bf16, lse_saved [Hq,S] fp32.
-    rope_base > 0 rotates Q and K at positions pos0 + s."""
+    """y [(B,)S,dm] bf16, o_saved [(B,)S,Hq,d] bf16, lse_saved [(B,)Hq,S]
+    fp32.  rope_base > 0 rotates Q and K at positions pos0 + s."""
     torch = _torch()
-    S, dm = x.shape
+    B, (S, dm) = _batch(x, 2)
     need = upipe_layer_fwd_workspace_size(S, dm, Hq, Hkv, d, U)
     if need == 0:
         raise UpipeError("upipe_layer_fwd_workspace_size", -1)
     if ws is None:
         ws = workspace(need, x.device)
     y = torch.empty_like(x)
-    o = torch.empty((S, Hq, d), dtype=torch.bfloat16, device=x.device)
-    lse = torch.empty((Hq, S), dtype=torch.float32, device=x.device)
+    lead = (B,) if x.dim() == 3 else ()
+    o = torch.empty(lead + (S, Hq, d), dtype=torch.bfloat16, device=x.device)
+    lse = torch.empty(lead + (Hq, S), dtype=torch.float32, device=x.device)
     bf = torch.bfloat16
     st = upipe_layer_fwd(_ptr(x, bf, "x"), _ptr(wqkv, bf, "wqkv"),
                          _ptr(wo, bf, "wo"), _ptr(y, bf, "y"),
                          _ptr(o, bf, "o_saved"),
                          _ptr(lse, torch.float32, "lse_saved"),
-                         S, dm, Hq, Hkv, d, U, float(rope_base), int(pos0),
+                         B, S, dm, Hq, Hkv, d, U, float(rope_base), int(pos0),
                          ws.data_ptr(), ws.numel(), _stream())
     _check("upipe_layer_fwd", st)
     return y, o, lse
@@ -349,11 +364,11 @@ def layer_fwd(x, wqkv, wo, Hq, Hkv, d=128, U=1, ws=None, rope_base=0.0, pos0=0):
 
 def layer_bwd(x, wqkv, wo, o_saved, lse_saved, dy, Hq, Hkv, d=128, U=1,
               ws=None, rope_base=0.0, pos0=0):
-    """dx [S,dm], dwqkv [dm,(Hq+2Hkv)d], dwo [Hq d, dm], all bf16.
-    o_saved = lse_saved = None recomputes the attention output (full
-    checkpointing) instead of reading the kept one."""
+    """dx [(B,)S,dm], dwqkv [dm,(Hq+2Hkv)d], dwo [Hq d, dm] (summed over the
+    batch), all bf16.  o_saved = lse_saved = None recomputes the attention
+    output (full checkpointing) instead of reading the kept one."""
     torch = _torch()
-    S, dm = x.shape
+    B, (S, dm) = _batch(x, 2)
     need = upipe_layer_bwd_workspace_size(S, dm, Hq, Hkv, d, U)
     if need == 0:
         raise UpipeError("upipe_layer_bwd_workspace_size", -1)
@@ -372,7 +387,7 @@ def layer_bwd(x, wqkv, wo, o_saved, lse_saved, dy, Hq, Hkv, d=128, U=1,
                          _ptr(lse_saved, torch.float32, "lse_saved") if kept else None,
                          _ptr(dy, bf, "dy"), _ptr(dx, bf, "dx"),
                          _ptr(dwqkv, bf, "dwqkv"), _ptr(dwo, bf, "dwo"),
-                         S, dm, Hq, Hkv, d, U, float(rope_base), int(pos0),
+                         B, S, dm, Hq, Hkv, d, U, float(rope_base), int(pos0),
                          ws.data_ptr(), ws.numel(), _stream())
     _check("upipe_layer_bwd", st)
     return dx, dwqkv, dwo

@@ -41,7 +41,7 @@ FAKE = 1 << 20   # a 16-byte aligned non-null address; never dereferenced
 
 
 def _fwd(**kw):
-    a = dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=FAKE, S=512, Hq=4, Hkv=1,
+    a = dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=FAKE, B=1, S=512, Hq=4, Hkv=1,
              d=128, causal=1, U=1, ws=FAKE, ws_bytes=1 << 40, stream=None)
     a.update(kw)
     return upipe.upipe_attn_fwd(*a.values())
@@ -49,7 +49,7 @@ def _fwd(**kw):
 
 def _bwd(**kw):
     a = dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=FAKE, dout=FAKE, dq=FAKE,
-             dk=FAKE, dv=FAKE, S=512, Hq=4, Hkv=1, d=128, causal=1, U=1,
+             dk=FAKE, dv=FAKE, B=1, S=512, Hq=4, Hkv=1, d=128, causal=1, U=1,
              ws=FAKE, ws_bytes=1 << 40, stream=None)
     a.update(kw)
     return upipe.upipe_attn_bwd(*a.values())
@@ -69,6 +69,9 @@ def test_argument_validation(fn):
     assert fn(ws=None) == INV
     assert fn(causal=2) == INV
     assert fn(ws_bytes=1024) == WS
+    assert fn(B=0) == INV
+    assert fn(B=-1) == INV
+    assert fn(B=8, ws_bytes=1024) == WS       # a batch needs no more workspace
 
 
 def _ring(**kw):
@@ -161,19 +164,21 @@ def test_layer_entry_points_validate():
     S, dm = 256, 512
     assert upipe.upipe_layer_fwd_workspace_size(S, 500, 4, 1, 128, 1) == 0
     assert upipe.upipe_layer_fwd_workspace_size(S, dm, 4, 1, 64, 1) == 0
-    assert upipe.upipe_layer_fwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, S, dm, 4,
+    assert upipe.upipe_layer_fwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, S, dm, 4,
                                  1, 128, 3, 0.0, 0, FAKE, 1 << 40, None) == -1
+    assert upipe.upipe_layer_fwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0, S, dm, 4,
+                                 1, 128, 1, 0.0, 0, FAKE, 1 << 40, None) == -1   # B = 0
 
 
 def _layer(fn, **kw):
-    a = dict(S=256, dm=512, Hq=4, Hkv=1, d=128, U=1, base=5e5, pos0=0)
+    a = dict(B=1, S=256, dm=512, Hq=4, Hkv=1, d=128, U=1, base=5e5, pos0=0)
     a.update(kw)
     if fn == "fwd":
-        return upipe.upipe_layer_fwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, a["S"], a["dm"],
-                                     a["Hq"], a["Hkv"], a["d"], a["U"], a["base"], a["pos0"],
-                                     FAKE, 0, None)
+        return upipe.upipe_layer_fwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, a["B"], a["S"],
+                                     a["dm"], a["Hq"], a["Hkv"], a["d"], a["U"], a["base"],
+                                     a["pos0"], FAKE, 0, None)
     return upipe.upipe_layer_bwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
-                                 a["S"], a["dm"], a["Hq"], a["Hkv"], a["d"], a["U"],
+                                 a["B"], a["S"], a["dm"], a["Hq"], a["Hkv"], a["d"], a["U"],
                                  a["base"], a["pos0"], FAKE, 0, None)
 
 
@@ -188,6 +193,9 @@ def test_layer_rope_arguments_validate(fn):
     assert _layer(fn, pos0=-1) == UNS
     assert _layer(fn, pos0=(1 << 32) - 256) == WS   # last row at 2^32 - 1
     assert _layer(fn, pos0=(1 << 32) - 255) == UNS
+    assert _layer(fn, B=4) == WS                 # a batch: same workspace
+    assert _layer(fn, B=0) == INV
+    assert _layer(fn, B=-3) == INV
 
 
 def test_layer_bwd_saved_output_both_or_neither():
@@ -195,8 +203,8 @@ def test_layer_bwd_saved_output_both_or_neither():
     S, dm = 256, 512
 
     def bwd(o, lse):
-        return upipe.upipe_layer_bwd(FAKE, FAKE, FAKE, o, lse, FAKE, FAKE, FAKE, FAKE, S, dm, 4,
-                                     1, 128, 1, 0.0, 0, FAKE, 0, None)
+        return upipe.upipe_layer_bwd(FAKE, FAKE, FAKE, o, lse, FAKE, FAKE, FAKE, FAKE, 1, S, dm,
+                                     4, 1, 128, 1, 0.0, 0, FAKE, 0, None)
     assert bwd(FAKE, FAKE) == WS           # kept output (selective checkpointing)
     assert bwd(None, None) == WS           # recomputed (full checkpointing)
     assert bwd(FAKE, None) == INV

@@ -102,6 +102,27 @@ def layer_inputs(S, d_model, Hq, Hkv, d, seed, w_std=0.02):
     return x, wqkv, wo, dy
 
 
+def batch_attention_inputs(S, Hq, Hkv, d, seed, B):
+    """q, k, v, do [B, S, H, d]: sequence b drawn as attention_inputs with seed
+    + b (B = 1 gives attention_inputs itself, with a leading batch of 1)."""
+    seqs = [attention_inputs(S, Hq, Hkv, d, seed + b) for b in range(B)]
+    return tuple(torch.stack([t[i] for t in seqs]) for i in range(4))
+
+
+def batch_layer_inputs(S, d_model, Hq, Hkv, d, seed, B, w_std=0.02):
+    """x [B, S, dm], wqkv, wo (shared), dy [B, S, dm]: sequence b's x and dy are
+    those of layer_inputs with seed + b."""
+    xs, dys = [], []
+    wqkv = wo = None
+    for b in range(B):
+        x, wq, wo_b, dy = layer_inputs(S, d_model, Hq, Hkv, d, seed + b, w_std)
+        if b == 0:
+            wqkv, wo = wq, wo_b
+        xs.append(x)
+        dys.append(dy)
+    return torch.stack(xs), wqkv, wo, torch.stack(dys)
+
+
 def ring_inputs(w: Workload):
     """q [S,Hq,d] (the query block), k, v [kv_len,Hkv,d] (the key block)."""
     gen = torch.Generator(device="cpu").manual_seed(w.seed)
