@@ -111,9 +111,30 @@ __global__ __launch_bounds__(256, 3 - GemmStages<EPI>::N) void gemm_kernel(
   const int r32 = lane & 31, g = lane >> 5;
   const int wm = w >> 1, wn = w & 1;
   const int64_t tiles_n = N / BN;
-  const int64_t tile = blockIdx.x;
+  // Workgroups are dispatched round-robin over the 8 XCDs, each with its own
+  // L2; which tile a workgroup computes is a permutation chosen per product
+  // (the results do not depend on it):
+  //   HEADS   (long k, a few weight columns): every XCD takes a contiguous
+  //           run of tiles, m-major, so the activation rows are fetched once;
+  //   PARTIAL (split-K weight gradients): every XCD takes whole splits, and
+  //           walks a split along its shorter side first (the tiles that
+  //           share the wider operand's block run together);
+  //   ACC32   (short k, many weight columns): round-robin, so each XCD keeps
+  //           an eighth of the weight columns in its L2.
+  int64_t tile = blockIdx.x, split = blockIdx.y;
+  if (EPI != GEMM_EPI_ACC32) {
+    const int64_t nx = gridDim.x;
+    const int64_t d = (int64_t)blockIdx.y * nx + blockIdx.x;   // dispatch order
+    const int64_t nwg = nx * gridDim.y, xcd = d % 8, slot = d / 8;
+    const int64_t per = nwg / 8, rem = nwg % 8;
+    const int64_t L = xcd < rem ? xcd * (per + 1) + slot : rem * (per + 1) + (xcd - rem) * per + slot;
+    tile = L % nx;
+    split = L / nx;
+    const int64_t tiles_m = M / BM;
+    if (EPI == GEMM_EPI_PARTIAL && tiles_m < tiles_n)   // m fastest
+      tile = (tile % tiles_m) * tiles_n + tile / tiles_m;
+  }
   const int64_t m0 = (tile / tiles_n) * BM, n0 = (tile % tiles_n) * BN;
-  const int64_t split = blockIdx.y;
   const int64_t kb0 = k_begin + split * k_len;
   int64_t kend = kb0 + k_len;
   if (kend > k_begin + E.k_total) kend = k_begin + E.k_total;
