@@ -55,7 +55,7 @@ Profiler& prof() {
 const char* const kFamilyNames[] = {
     "pack_rows",      "unpack_rows",   "rowdot_lse",     "attn_fwd",
     "attn_bwd_dkdv",  "attn_bwd_dq",   "gemm",           "gemm_wgrad",
-    "reduce_splitk",  "lse_merge",     "rope",
+    "reduce_splitk",  "lse_merge",     "rope",           "split_merge",
 };
 const int kNumFamilies = sizeof(kFamilyNames) / sizeof(kFamilyNames[0]);
 
@@ -115,7 +115,9 @@ AttnFwdPlan plan_attn_fwd_ring(int64_t Sq, int64_t Skv, int Hq, int Hkv, int U) 
   p.Kp = c.take(Hkv * kvhead);
   p.Vp = c.take(Hkv * kvhead);
   p.Qc = c.take(U * qhead);
-  p.Oc = c.take(U * qhead);
+  p.ns = attn_fwd_key_splits(p.Sp, p.Skvp);
+  p.Oc = c.take(p.ns * U * qhead);
+  if (p.ns > 1) p.lse_part = c.take((size_t)p.ns * U * p.Sp * 4);
   p.total = c.used;
   return p;
 }
@@ -163,8 +165,23 @@ int run_attn_fwd_ring(const bf16* q, const bf16* k, const bf16* v, bf16* o, floa
   UPIPE_LAUNCH(kPackRows, st, launch_pack_rows(v, Skv, Hkv, 0, Hkv, p.Skvp, Vp, st));
   for (int h0 = 0; h0 < Hq; h0 += U) {
     UPIPE_LAUNCH(kPackRows, st, launch_pack_rows(q, Sq, Hq, h0, U, p.Sp, Qc, st));
-    UPIPE_LAUNCH(kAttnFwd, st, launch_attn_fwd(Qc, Kp, Vp, Oc, lse, Sq, p.Sp, Skv, p.Skvp, delta, U,
-                                               h0, G, causal, st));
+    if (p.ns == 1) {
+      UPIPE_LAUNCH(kAttnFwd, st, launch_attn_fwd(Qc, Kp, Vp, Oc, lse, Sq, p.Sp, Skv, p.Skvp, delta,
+                                                 U, h0, G, causal, st));
+    } else {
+      // Two key halves per query block (the grid would otherwise leave CUs
+      // idle), merged like two ring steps: rows [U][Sp] as one head.
+      float* lp = (float*)(ws + p.lse_part);
+      const int64_t rows = (int64_t)U * p.Sp;
+      UPIPE_LAUNCH(kAttnFwd, st,
+                   launch_attn_fwd_split(Qc, Kp, Vp, Oc, lp, Sq, p.Sp, Skv, p.Skvp, delta, U, h0,
+                                         G, causal, p.ns, 0, p.Sp, p.Sp, st));
+      UPIPE_LAUNCH(kSplitMerge, st,
+                   launch_lse_merge(Oc, lp, Oc + rows * HEAD_DIM, lp + rows, rows, 1, st));
+      UPIPE_LAUNCH(kUnpackRows, st,
+                   hipMemcpy2DAsync(lse + (int64_t)h0 * Sq, Sq * 4, lp, p.Sp * 4, Sq * 4, U,
+                                    hipMemcpyDeviceToDevice, st));
+    }
     UPIPE_LAUNCH(kUnpackRows, st, launch_unpack_rows(Oc, Sq, Hq, h0, U, p.Sp, o, st));
   }
   return UPIPE_OK;

@@ -27,6 +27,7 @@ enum Family {
   kReduceSplitk,
   kLseMerge,
   kRope,
+  kSplitMerge,
 };
 
 // Records HIP events around one launch when profiling is on.
@@ -66,7 +67,8 @@ struct Carver {
 struct AttnFwdPlan {
   int64_t Sp = 0;     // query rows, padded
   int64_t Skvp = 0;   // key/value rows, padded
-  size_t Kp = 0, Vp = 0, Qc = 0, Oc = 0, total = 0;
+  int ns = 1;         // key splits per query block (their partial results are merged)
+  size_t Kp = 0, Vp = 0, Qc = 0, Oc = 0, lse_part = 0, total = 0;
 };
 
 struct AttnBwdPlan {

@@ -82,15 +82,17 @@ template <bool CAUSAL>
 __global__ __launch_bounds__(512, 1) void attn_fwd_kernel(
     const bf16* __restrict__ Qc, const bf16* __restrict__ Kp, const bf16* __restrict__ Vp,
     bf16* __restrict__ Oc, float* __restrict__ lse, int Sq, int Sqp, int Skv, int Skvp, int delta,
-    int U, int h0, int G, int nqb) {
+    int U, int h0, int G, int nqb, int ns, int lse_h0, int lse_ld, int lse_rows) {
   __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
   const int t = threadIdx.x;
   const int lane = t & 63;
   const int w = __builtin_amdgcn_readfirstlane(t >> 6);
   const int r32 = lane & 31, g = lane >> 5;
+  // Workgroup -> (query block, head, key split), longest blocks first.
   const int L = blockIdx.x;
-  const int qb = nqb - 1 - L / U;
-  const int u = L % U;
+  const int qb = nqb - 1 - L / (U * ns);
+  const int u = (L % (U * ns)) / ns;
+  const int sp = L % ns;
   const int kvh = (h0 + u) / G;
   const int q0 = qb * BQ;
   const int qw = q0 + 32 * w;               // first query row of this wave
@@ -118,7 +120,10 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_kernel(
   // Last visible key of this lane's row and of the wave's first row.
   const int lim = CAUSAL ? min(myq + delta, Skv - 1) : Skv - 1;
   const int lim_w = CAUSAL ? min(qw + delta, Skv - 1) : Skv - 1;
-  if (nst > 0) issue_tile(rk, rv, offk, offv, 0, smem, w);
+  // This split's stages [j0, j1) of the block's nst (all of them when ns = 1).
+  const int per = (nst + ns - 1) / ns;
+  const int j0 = min(nst, sp * per), j1 = min(nst, j0 + per);
+  if (j0 < j1) issue_tile(rk, rv, offk, offv, j0 * BKS, smem + (j0 & 1) * STAGE, w);
 
   // Q^T B-operand fragments for the whole key loop: lane = query column,
   // k-group g covers head-dim [16s + 8g, 16s + 8g + 8).
@@ -145,12 +150,12 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_kernel(
   float l_run = 0.f;         // this lane's partial row sum
   const float sl2 = 1.4426950408889634f * 0.08838834764831845f;  // log2(e)/sqrt(128)
 
-  for (int j = 0; j < nst; ++j) {
+  for (int j = j0; j < j1; ++j) {
     const int ks = j * BKS;
     char* buf = smem + (j & 1) * STAGE;
     wait_vmem();
     __syncthreads();   // stage j landed for all waves; stage j-1's buffer is free
-    if (j + 1 < nst) issue_tile(rk, rv, offk, offv, ks + BKS, smem + ((j + 1) & 1) * STAGE, w);
+    if (j + 1 < j1) issue_tile(rk, rv, offk, offv, ks + BKS, smem + ((j + 1) & 1) * STAGE, w);
     if (j >= nw) continue;                  // whole stage masked for this wave
     {
       const int kb = ks;
@@ -206,7 +211,7 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_kernel(
   if (!rows_ok) return;
   const float l_tot = l_run + __shfl_xor(l_run, 32);
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;   // no visible key: O = 0
-  bf16* op = Oc + ((int64_t)u * Sqp + myq) * HEAD_DIM + 4 * g;
+  bf16* op = Oc + ((int64_t)(sp * U + u) * Sqp + myq) * HEAD_DIM + 4 * g;
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
@@ -216,27 +221,44 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_kernel(
       for (int b = 0; b < 4; ++b) ov[b] = (bf16)(oacc[dt][4 * a + b] * inv);
       *reinterpret_cast<bf16x4*>(op + 32 * dt + 8 * a) = ov;
     }
-  if (g == 0 && myq < Sq)
-    lse[(int64_t)(h0 + u) * Sq + myq] =
+  if (g == 0 && myq < lse_rows)
+    lse[(int64_t)(lse_h0 + sp * U + u) * lse_ld + myq] =
         l_tot > 0.f ? (m_ref + __log2f(l_tot)) * 0.6931471805599453f : -INFINITY;
 }
 
 }  // namespace
 
-hipError_t launch_attn_fwd(const bf16* Qc, const bf16* Kp, const bf16* Vp, bf16* Oc, float* lse,
-                           int64_t Sq, int64_t Sqp, int64_t Skv, int64_t Skvp, int64_t delta, int U,
-                           int h0, int G, int causal, hipStream_t st) {
+hipError_t launch_attn_fwd_split(const bf16* Qc, const bf16* Kp, const bf16* Vp, bf16* Oc,
+                                 float* lse, int64_t Sq, int64_t Sqp, int64_t Skv, int64_t Skvp,
+                                 int64_t delta, int U, int h0, int G, int causal, int ns,
+                                 int lse_h0, int64_t lse_ld, int64_t lse_rows, hipStream_t st) {
   const int nqb = (int)((Sqp + BQ - 1) / BQ);
   // Offsets beyond either length change nothing: clamp into int range.
   const int dl = (int)(delta < -Sq ? -Sq : delta > Skv ? Skv : delta);
-  dim3 grid((unsigned)(nqb * U));
+  dim3 grid((unsigned)(nqb * U * ns));
   if (causal)
     hipLaunchKernelGGL(attn_fwd_kernel<true>, grid, dim3(512), 0, st, Qc, Kp, Vp, Oc, lse, (int)Sq,
-                       (int)Sqp, (int)Skv, (int)Skvp, dl, U, h0, G, nqb);
+                       (int)Sqp, (int)Skv, (int)Skvp, dl, U, h0, G, nqb, ns, lse_h0, (int)lse_ld,
+                       (int)lse_rows);
   else
     hipLaunchKernelGGL(attn_fwd_kernel<false>, grid, dim3(512), 0, st, Qc, Kp, Vp, Oc, lse, (int)Sq,
-                       (int)Sqp, (int)Skv, (int)Skvp, dl, U, h0, G, nqb);
+                       (int)Sqp, (int)Skv, (int)Skvp, dl, U, h0, G, nqb, ns, lse_h0, (int)lse_ld,
+                       (int)lse_rows);
   return hipGetLastError();
+}
+
+hipError_t launch_attn_fwd(const bf16* Qc, const bf16* Kp, const bf16* Vp, bf16* Oc, float* lse,
+                           int64_t Sq, int64_t Sqp, int64_t Skv, int64_t Skvp, int64_t delta, int U,
+                           int h0, int G, int causal, hipStream_t st) {
+  return launch_attn_fwd_split(Qc, Kp, Vp, Oc, lse, Sq, Sqp, Skv, Skvp, delta, U, h0, G, causal, 1,
+                               h0, Sq, Sq, st);
+}
+
+int attn_fwd_key_splits(int64_t Sqp, int64_t Skvp) {
+  // Fewer 256-row query blocks than half the CUs leave CUs idle at U = 1:
+  // split the key range of every block in two (a function of the lengths
+  // only, so that every chunk size U gives the same results).
+  return ((Sqp + BQ - 1) / BQ <= 128 && Skvp / BKS >= 2) ? 2 : 1;
 }
 
 }  // namespace upipe

@@ -34,6 +34,16 @@ hipError_t launch_attn_fwd(const bf16* Qc, const bf16* Kp, const bf16* Vp,
                            bf16* Oc, float* lse, int64_t Sq, int64_t Sqp,
                            int64_t Skv, int64_t Skvp, int64_t delta, int U,
                            int h0, int G, int causal, hipStream_t st);
+// The same with the key range of every query block cut into `ns` splits of
+// equal stage counts, split s writing O to Oc + s U Sqp d ([ns][U][Sqp][d])
+// and lse row (lse_h0 + s U + u) of leading dimension lse_ld, rows i <
+// lse_rows (the plain call: ns = 1, lse_h0 = h0, lse_ld = lse_rows = Sq).
+hipError_t launch_attn_fwd_split(const bf16* Qc, const bf16* Kp, const bf16* Vp, bf16* Oc,
+                                 float* lse, int64_t Sq, int64_t Sqp, int64_t Skv, int64_t Skvp,
+                                 int64_t delta, int U, int h0, int G, int causal, int ns,
+                                 int lse_h0, int64_t lse_ld, int64_t lse_rows, hipStream_t st);
+// Number of key splits the forward uses for these padded lengths (1 or 2).
+int attn_fwd_key_splits(int64_t Sqp, int64_t Skvp);
 // In place, per row (s, h) of o [S, H, d] and lse [H, S]: fold the partial
 // result (o_p, lse_p) over a disjoint key set into (o, lse).
 hipError_t launch_lse_merge(bf16* o, float* lse, const bf16* o_p,

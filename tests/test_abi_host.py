@@ -95,11 +95,17 @@ def test_ring_step_validation_and_workspace():
     assert _ring(k=None) == INV
     assert _ring(lse=FAKE + 4) == INV
     assert _ring(ws_bytes=1024) == WS
-    # K, V packed at the key length; Q, O chunk buffers at the query length
+    # K, V packed at the key length; Q, O chunk buffers at the query length.
+    # Few query blocks (at most 128 of 256 rows) and at least two key stages:
+    # the key range is split in two, with a second O buffer and fp32 lse rows
+    # for both halves.
     qh, kh = 512 * 128 * 2, 384 * 128 * 2
     for U in (1, 2, 4):
         assert upipe.upipe_attn_fwd_ring_workspace_size(512, 384, 4, 1, 128, U) == \
-            2 * kh + 2 * U * qh
+            2 * kh + U * qh + 2 * U * qh + 2 * U * 512 * 4
+    # a single key stage: no split
+    assert upipe.upipe_attn_fwd_ring_workspace_size(512, 128, 4, 1, 128, 1) == \
+        2 * 128 * 256 + 2 * qh
     # equal lengths: the plain forward's workspace
     assert upipe.upipe_attn_fwd_ring_workspace_size(1000, 1000, 4, 2, 128, 2) == \
         upipe.upipe_attn_fwd_workspace_size(1000, 4, 2, 128, 2)
@@ -127,8 +133,15 @@ def test_workspace_sizes_follow_the_plan():
         carry = 4 * head if U < 4 else 0          # fp32 dK, dV accumulators
         # K, V resident; per chunk head Q, dO, dQ and the fp32 D and lse rows
         assert bwd == 2 * head + carry + 3 * U * head + 2 * U * Sp * 4
-    # padding of a ragged length to the 128-row granule
+    # padding of a ragged length to the 128-row granule (one key stage: no split)
     assert upipe.upipe_attn_fwd_workspace_size(1, 1, 1, d, 1) == 4 * 128 * d * 2
+    # 32768 rows = 128 query blocks of 256: keys split in two; one row more
+    # makes 129 blocks: no split
+    s32 = 32768 * d * 2
+    assert upipe.upipe_attn_fwd_workspace_size(32768, 4, 1, d, 1) == \
+        2 * s32 + s32 + 2 * s32 + 2 * 32768 * 4
+    s33 = 32896 * d * 2
+    assert upipe.upipe_attn_fwd_workspace_size(32769, 4, 1, d, 1) == 2 * s33 + 2 * s33
     assert upipe.upipe_attn_fwd_workspace_size(0, 1, 1, d, 1) == 0
     assert upipe.upipe_attn_fwd_workspace_size(5, 4, 1, 64, 1) == 0
     # longest supported share: 2^24 - 128 rows (32-bit per-head byte offsets)
