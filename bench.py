@@ -94,6 +94,29 @@ def measured_traffic(kernel, workload, U):
     return rec["fetch_bytes"] + rec["write_bytes"]
 
 
+def host_info():
+    """(BLAS threads in use, BLAS library, CPU model) of this host."""
+    cores, blas = os.cpu_count(), "unknown"
+    try:
+        from threadpoolctl import threadpool_info
+        info = [i for i in threadpool_info() if i.get("user_api") == "blas"] or threadpool_info()
+        if info:
+            cores = max(i.get("num_threads", 1) for i in info)
+            blas = ",".join(sorted({str(i.get("internal_api", "?")) for i in info}))
+    except Exception:  # pragma: no cover
+        pass
+    cpu = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    cpu = line.split(":", 1)[1].strip()
+                    break
+    except OSError:  # pragma: no cover
+        pass
+    return cores, blas, cpu
+
+
 def cpu_baseline(w, q, k, v, do, target_s):
     """Oracle (float64 numpy) on a bounded causal prefix of the workload.
 
@@ -104,11 +127,7 @@ def cpu_baseline(w, q, k, v, do, target_s):
     """
     import numpy as np
     from oracle import attention as A
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:  # pragma: no cover
-        cores = os.cpu_count()
+    cores, blas, cpu = host_info()
 
     def run(sp):
         f = lambda t, h: t[:sp, :h].float().double().numpy()  # noqa: E731
@@ -132,7 +151,7 @@ def cpu_baseline(w, q, k, v, do, target_s):
     flops = 3.5 * 4 * w.d * pairs
     full_pairs = w.S * (w.S + 1) // 2 * w.Hq
     return {"value": round(flops / t / 1e12, 6), "unit": "TFLOP/s",
-            "cores": cores, "kind": "oracle",
+            "cores": cores, "kind": "oracle", "blas": blas, "cpu": cpu,
             "sample": f"causal prefix S'={sp} of {w.name}, 1 query head "
                       f"(kv head 0), fwd+bwd, float64 numpy, {t:.1f} s",
             "extrapolated_full_s": round(t * full_pairs / pairs, 1),
@@ -307,8 +326,8 @@ def main():
         out["peak_activation_model_gb_vs_U"] = {
             str(u): round(workspace_model_gb(S, Hq, Hkv, d, u), 4) for u in w.U_sweep}
         us = [int(u) for u in sweep_mem]
-        A, B, r2 = linear_fit(us, [sweep_mem[str(u)] for u in us])
-        out["peak_activation_fit"] = {"A_gb": round(A, 4), "B_gb_per_U": round(B, 4),
+        fit_a, fit_b, r2 = linear_fit(us, [sweep_mem[str(u)] for u in us])
+        out["peak_activation_fit"] = {"A_gb": round(fit_a, 4), "B_gb_per_U": round(fit_b, 4),
                                       "r2": round(r2, 4)}
         out["peak_activation_note"] = (
             "max_memory_allocated during one fwd+bwd above the resident "
@@ -344,13 +363,9 @@ def ring_cpu_baseline(w, q, k, v, delta, target_s):
         n = int(min(w.S, w.extra["kv_len"], max(n + 128, n * (target_s / max(t, 1e-3)) ** 0.5)))
         t = run(n)
     pairs = W.ring_pairs(n, n, delta)
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:  # pragma: no cover
-        cores = os.cpu_count()
+    cores, blas, cpu = host_info()
     return {"value": round(4 * w.d * pairs / t / 1e12, 6), "unit": "TFLOP/s", "cores": cores,
-            "kind": "oracle",
+            "kind": "oracle", "blas": blas, "cpu": cpu,
             "sample": f"first {n} query rows x first {n} keys of {w.name}, 1 query head, "
                       f"ring-step forward, float64 numpy, {t:.1f} s"}
 
