@@ -30,8 +30,9 @@
  *    (bidirectional) attention over all S keys.
  *  - Determinism: for fixed shapes every output is bitwise identical across
  *    calls and across every valid U (one fixed reduction order: query heads
- *    ascending, then query blocks ascending; fp32 partial sums are carried
- *    between chunks through the workspace).
+ *    ascending, then query tiles descending; fp32 partial sums are carried
+ *    between chunks through the workspace; whether the forward splits a
+ *    query block's key range in two depends on the lengths only).
  *  - Errors: arguments are validated on the host before anything is
  *    enqueued; a failing call enqueues nothing and returns a negative
  *    upipe_status.  A launch failure returns UPIPE_ERR_HIP (work queued
