@@ -92,26 +92,38 @@ __device__ __forceinline__ void read_dvdk(const char* buf, int sub, int lane, Fr
     }
 }
 
-// S^T and dP^T of one subtile from its fragments (16 MFMAs).
+// S^T and D - dP^T of one subtile from its fragments (16 MFMAs).  The dP
+// accumulators start from the staged D rows (loaded straight into them) and
+// the value fragments come negated, so the chain ends at D - dP and dS needs
+// no subtraction: P (D - dP) = -dS.
 __device__ __forceinline__ void subtile_sdp(const Frags& fr, const bf16x8 (&kf)[8],
-                                            const bf16x8 (&vf)[8], f32x16& sacc, f32x16& pacc) {
+                                            const bf16x8 (&nvf)[8], const char* buf, int sub,
+                                            int g, f32x16& sacc, f32x16& pacc) {
+  const float* Dl = reinterpret_cast<const float*>(buf + OFF_D) + sub;
 #pragma unroll
-  for (int i = 0; i < 16; ++i) { sacc[i] = 0.f; pacc[i] = 0.f; }
+  for (int a = 0; a < 4; ++a) {
+    const f32x4 d4 = *reinterpret_cast<const f32x4*>(Dl + 8 * a + 4 * g);
+#pragma unroll
+    for (int b = 0; b < 4; ++b) pacc[4 * a + b] = d4[b];
+  }
+#pragma unroll
+  for (int i = 0; i < 16; ++i) sacc[i] = 0.f;
 #pragma unroll
   for (int s = 0; s < 8; ++s) {
     sacc = mfma32x32x16(fr.f[2 * s], kf[s], sacc);
-    pacc = mfma32x32x16(fr.f[2 * s + 1], vf[s], pacc);
+    pacc = mfma32x32x16(fr.f[2 * s + 1], nvf[s], pacc);
   }
 }
 
-// P and dS of one subtile (rows `sub`.. of the tile, first row qs) as bf16 A
-// operands, from its scores and the staged lse / D rows.
+// P and -dS of one subtile (rows `sub`.. of the tile, first row qs) as bf16 A
+// operands, from its scores, the staged lse rows and D - dP.  Negation is
+// exact and commutes with rounding, so the dK accumulators carry exactly -dK
+// (the final scale is -1/sqrt d).
 template <bool CAUSAL>
 __device__ __forceinline__ void subtile_pds(const f32x16& sacc, const f32x16& pacc, const char* buf,
                                             int sub, uint32_t qs, uint32_t mykey, bool diag, int g,
                                             bf16x8 (&pf)[2], bf16x8 (&sf)[2]) {
   const float* lsel = reinterpret_cast<const float*>(buf + OFF_LSE) + sub;
-  const float* Dl = reinterpret_cast<const float*>(buf + OFF_D) + sub;
   float p[16];
 #pragma unroll
   for (int a = 0; a < 4; ++a) {
@@ -125,14 +137,9 @@ __device__ __forceinline__ void subtile_pds(const f32x16& sacc, const f32x16& pa
       if (mykey > qs + 8 * (i >> 2) + 4 * g + (i & 3)) p[i] = 0.f;
   }
 #pragma unroll
-  for (int a = 0; a < 4; ++a) {
-    const f32x4 d4 = *reinterpret_cast<const f32x4*>(Dl + 8 * a + 4 * g);
-#pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const int i = 4 * a + b;
-      pf[i >> 3][i & 7] = (bf16)p[i];
-      sf[i >> 3][i & 7] = (bf16)(p[i] * (pacc[i] - d4[b]));
-    }
+  for (int i = 0; i < 16; ++i) {
+    pf[i >> 3][i & 7] = (bf16)p[i];
+    sf[i >> 3][i & 7] = (bf16)(p[i] * pacc[i]);
   }
 }
 
@@ -184,10 +191,10 @@ __device__ __forceinline__ void pair_step(const char* buf, int base, uint32_t qb
   read_sdp(buf, base + 32, r32, g, fa);
   read_sdp(buf, base, r32, g, fb);
   __builtin_amdgcn_sched_barrier(0);
-  subtile_sdp(fa, kf, vf, s1, p1);                                            // A
+  subtile_sdp(fa, kf, vf, buf, base + 32, g, s1, p1);                                            // A
   read_dvdk(buf, base + 32, lane, fa);
   __builtin_amdgcn_sched_barrier(0);
-  subtile_sdp(fb, kf, vf, s0, p0);                                            // B
+  subtile_sdp(fb, kf, vf, buf, base, g, s0, p0);                                            // B
   subtile_pds<CAUSAL>(s1, p1, buf, base + 32, q1, mykey, q1 < kw + 31, g, pf1, sf1);
   read_dvdk(buf, base, lane, fb);
   interleave_mfma_valu();
@@ -245,7 +252,8 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(
   QStageSrc cur = srcs(hlo);
   issue_qstage(cur, offr, (nqt - 1) * QT, smem, w, lane);
 
-  // K and V B-operand fragments (lane = key column, k = head dim).
+  // K and -V B-operand fragments (lane = key column, k = head dim); -V makes
+  // the dP products count down from D.
   bf16x8 kf[8], vf[8];
   {
     const bf16* kp = Kp + ((int64_t)kvh * Sp + mykey) * HEAD_DIM + 8 * g;
@@ -253,7 +261,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
       kf[s] = *reinterpret_cast<const bf16x8*>(kp + 16 * s);
-      vf[s] = *reinterpret_cast<const bf16x8*>(vp + 16 * s);
+      vf[s] = -*reinterpret_cast<const bf16x8*>(vp + 16 * s);
     }
   }
 
@@ -319,7 +327,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(
         const uint32_t key = kw + 8 * (i >> 2) + 4 * g + (i & 3);
         if (key < (uint64_t)S) {
           const int64_t off = (int64_t)key * kv_row + kvh * kv_head + 32 * dt + r32;
-          dk[off] = (bf16)(dka[dt][i] * kScale);
+          dk[off] = (bf16)(dka[dt][i] * -kScale);
           dv[off] = (bf16)dva[dt][i];
         }
       }

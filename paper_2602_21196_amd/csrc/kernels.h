@@ -53,8 +53,9 @@ hipError_t launch_lse_merge(bf16* o, float* lse, const bf16* o_p,
 // ---- attention backward (attn_bwd.hip) -----------------------------------
 // lse_c below holds log2(e) * lse (the kernels evaluate exp2).
 // Key/value gradients of the chunk's heads, accumulated in fp32 on top of
-// dK32/dV32 [Hkv, Sp, d] (read unless the chunk holds a group's first head),
-// written back there, or -- when the chunk holds the group's last head --
+// dK32/dV32 [Hkv, Sp, d] (read unless the chunk holds a group's first head;
+// dK32 carries the unscaled sum with its sign flipped, -sum dS^T Q), written
+// back there, or -- when the chunk holds the group's last head --
 // scaled and rounded into dk/dv bf16: row s of key/value head g at element
 // s * kv_row + g * kv_head (token-major [S, Hkv, d]: kv_row = Hkv * d,
 // kv_head = d; head-major [Hkv, Sp, d]: kv_row = d, kv_head = Sp * d).
