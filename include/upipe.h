@@ -40,7 +40,9 @@
  *    next synchronisation.  No C++ exception crosses this interface.
  *  - Supported shapes: d == 128; S >= 1 (any length: rows past the last tile
  *    are padded inside the workspace); 1 <= Hkv <= Hq, Hkv | Hq; 1 <= U,
- *    U | Hq; Hq <= 64; S * max(Hq, d_model/128) * d < 2^40.
+ *    U | Hq; Hq <= 64; S * max(Hq, d_model/128) * d < 2^40.  A batch of B
+ *    sequences needs B >= 1 and B times one sequence's largest tensor below
+ *    2^61 elements (UPIPE_ERR_INVALID_ARG otherwise).
  *  - Thread safety: calls are reentrant across host threads and streams as
  *    long as each concurrent call has its own workspace and outputs.  The
  *    profiling switch below is process-global and not thread-safe.
@@ -143,7 +145,8 @@ int upipe_attn_fwd(const void* q, const void* k, const void* v, void* o,
  * q_offset + i; with causal = 0 every key is.  A row that sees no key gets
  * o = 0 and lse = -inf (the empty set, neutral for the merge).  Head chunking
  * by U as for upipe_attn_fwd; with Sq = Skv and q_offset = kv_offset this is
- * upipe_attn_fwd.  |offsets| <= 2^62; workspace from
+ * upipe_attn_fwd.  |offsets| <= 2^62 and q_offset - kv_offset < 2^63
+ * (UPIPE_ERR_INVALID_ARG otherwise); workspace from
  * upipe_attn_fwd_ring_workspace_size (0 for invalid shapes).
  * ---------------------------------------------------------------------- */
 size_t upipe_attn_fwd_ring_workspace_size(int64_t Sq, int64_t Skv, int Hq, int Hkv,

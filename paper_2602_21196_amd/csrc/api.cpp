@@ -289,9 +289,9 @@ int upipe_attn_fwd(const void* q, const void* k, const void* v, void* o,
                    float* lse, int64_t B, int64_t S, int Hq, int Hkv, int d, int causal,
                    int U, void* ws, size_t ws_bytes, hipStream_t stream) {
   try {
-    if (B < 1) return UPIPE_ERR_INVALID_ARG;
     int rc = check_attn_shape(S, Hq, Hkv, d, U);
     if (rc != UPIPE_OK) return rc;
+    if (!batch_ok(B, S * Hq * HEAD_DIM)) return UPIPE_ERR_INVALID_ARG;
     if (causal != 0 && causal != 1) return UPIPE_ERR_INVALID_ARG;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) ||
         !aligned16(lse) || !aligned16(ws))
@@ -333,9 +333,11 @@ int upipe_attn_fwd_ring(const void* q, const void* k, const void* v, void* o, fl
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) ||
         !aligned16(lse) || !aligned16(ws))
       return UPIPE_ERR_INVALID_ARG;
+    int64_t delta;   // q_offset - kv_offset; fits unless it is exactly 2^63
+    if (__builtin_sub_overflow(q_offset, kv_offset, &delta)) return UPIPE_ERR_INVALID_ARG;
     if (ws_bytes < plan_attn_fwd_ring(Sq, Skv, Hq, Hkv, U).total) return UPIPE_ERR_WORKSPACE;
     return run_attn_fwd_ring((const bf16*)q, (const bf16*)k, (const bf16*)v, (bf16*)o, lse, Sq,
-                             Skv, q_offset - kv_offset, Hq, Hkv, causal, U, (char*)ws, stream);
+                             Skv, delta, Hq, Hkv, causal, U, (char*)ws, stream);
   } catch (...) {
     return UPIPE_ERR_HIP;
   }
@@ -382,9 +384,9 @@ int upipe_attn_bwd(const void* q, const void* k, const void* v, const void* o,
                    void* dv, int64_t B, int64_t S, int Hq, int Hkv, int d, int causal,
                    int U, void* ws, size_t ws_bytes, hipStream_t stream) {
   try {
-    if (B < 1) return UPIPE_ERR_INVALID_ARG;
     int rc = check_attn_shape(S, Hq, Hkv, d, U);
     if (rc != UPIPE_OK) return rc;
+    if (!batch_ok(B, S * Hq * HEAD_DIM)) return UPIPE_ERR_INVALID_ARG;
     if (causal != 0 && causal != 1) return UPIPE_ERR_INVALID_ARG;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) ||
         !aligned16(lse) || !aligned16(dout) || !aligned16(dq) || !aligned16(dk) ||

@@ -49,6 +49,11 @@ class ProfScope {
   } while (0)
 
 bool aligned16(const void* p);
+// B sequences of `per_seq` elements each address below 2^61 elements (so no
+// pointer offset into a batch can overflow); B >= 1.
+inline bool batch_ok(int64_t B, int64_t per_seq) {
+  return B >= 1 && per_seq >= 1 && B <= (int64_t(1) << 61) / per_seq;
+}
 // Rotary-embedding arguments from the ABI's (base, pos0) for rows 0..S-1:
 // base == 0 means no rotation; otherwise base must be finite and > 0
 // (UPIPE_ERR_INVALID_ARG) and positions pos0 .. pos0 + S - 1 must lie in

@@ -36,6 +36,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
+
 #include "../../include/upipe.h"
 #include "api_internal.h"
 #include "gemm.h"
@@ -355,9 +357,10 @@ int upipe_layer_fwd(const void* x, const void* wqkv, const void* wo, void* y, vo
                     int U, double rope_base, int64_t pos0, void* ws, size_t ws_bytes,
                     hipStream_t stream) {
   try {
-    if (B < 1) return UPIPE_ERR_INVALID_ARG;
     int rc = check_layer_shape(S, d_model, Hq, Hkv, d, U);
     if (rc != UPIPE_OK) return rc;
+    if (!batch_ok(B, S * std::max<int64_t>(d_model, (int64_t)Hq * HEAD_DIM)))
+      return UPIPE_ERR_INVALID_ARG;
     RopeArgs rope;
     rc = make_rope(rope_base, pos0, S, &rope);
     if (rc != UPIPE_OK) return rc;
@@ -379,9 +382,10 @@ int upipe_layer_bwd(const void* x, const void* wqkv, const void* wo, const void*
                     double rope_base, int64_t pos0, void* ws, size_t ws_bytes,
                     hipStream_t stream) {
   try {
-    if (B < 1) return UPIPE_ERR_INVALID_ARG;
     int rc = check_layer_shape(S, d_model, Hq, Hkv, d, U);
     if (rc != UPIPE_OK) return rc;
+    if (!batch_ok(B, S * std::max<int64_t>(d_model, (int64_t)Hq * HEAD_DIM)))
+      return UPIPE_ERR_INVALID_ARG;
     RopeArgs rope;
     rc = make_rope(rope_base, pos0, S, &rope);
     if (rc != UPIPE_OK) return rc;

@@ -72,6 +72,10 @@ def test_argument_validation(fn):
     assert fn(B=0) == INV
     assert fn(B=-1) == INV
     assert fn(B=8, ws_bytes=1024) == WS       # a batch needs no more workspace
+    # B times one sequence's [S, Hq, d] must stay below 2^61 elements
+    per_seq = 512 * 4 * 128
+    assert fn(B=(1 << 61) // per_seq, ws_bytes=1024) == WS
+    assert fn(B=(1 << 61) // per_seq + 1, ws_bytes=1024) == INV
 
 
 def _ring(**kw):
@@ -92,6 +96,10 @@ def test_ring_step_validation_and_workspace():
     assert _ring(causal=2) == INV
     assert _ring(q_offset=(1 << 62) + 1) == INV
     assert _ring(kv_offset=-(1 << 62) - 1) == INV
+    # the offset difference must fit in int64: 2^62 - (-2^62) = 2^63 does not
+    assert _ring(q_offset=1 << 62, kv_offset=-(1 << 62), ws_bytes=1024) == INV
+    assert _ring(q_offset=1 << 62, kv_offset=1 - (1 << 62), ws_bytes=1024) == WS
+    assert _ring(q_offset=-(1 << 62), kv_offset=1 << 62, ws_bytes=1024) == WS
     assert _ring(k=None) == INV
     assert _ring(lse=FAKE + 4) == INV
     assert _ring(ws_bytes=1024) == WS
@@ -209,6 +217,10 @@ def test_layer_rope_arguments_validate(fn):
     assert _layer(fn, B=4) == WS                 # a batch: same workspace
     assert _layer(fn, B=0) == INV
     assert _layer(fn, B=-3) == INV
+    # B times one sequence's largest tensor ([S, d_model] here) below 2^61
+    per_seq = 256 * 512
+    assert _layer(fn, B=(1 << 61) // per_seq) == WS
+    assert _layer(fn, B=(1 << 61) // per_seq + 1) == INV
 
 
 def test_layer_bwd_saved_output_both_or_neither():
