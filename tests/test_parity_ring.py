@@ -4,8 +4,10 @@
 Cases: query/key blocks of ragged lengths at negative, zero and positive
 offsets (rows that see no key, the diagonal, fully visible blocks),
 non-causal blocks, grouped heads and every chunk size U; the merge on random
-partials including empty rows; and full causal attention rebuilt on the GPU
-from ring steps over key blocks plus merges."""
+partials including empty rows; full causal attention rebuilt on the GPU
+from ring steps over key blocks plus merges; and the full-size ring step of
+the Llama3-8B share (32K queries against 32K keys, the forward's key range
+split in two), on sampled rows."""
 
 import numpy as np
 import pytest
@@ -130,3 +132,48 @@ def test_ring_decomposition_rebuilds_causal_attention(S, cuts):
     # against the GPU's own one-block forward: only bf16 rounding of the partials
     diff = (o_acc.cpu().float() - o_full.cpu()[qa:qb].float()).abs().max().item()
     assert diff <= 2.0 ** -6, diff
+
+
+@pytest.mark.timeout(300)
+def test_llama8b_ring_step_sampled():
+    """The ring step bench.py times (a 32K query block against the preceding
+    32K key/value block, Llama3-8B share split four ways), in the launch
+    configuration it times: bitwise equal across U; sampled rows of the
+    step and of its merge into the block's own causal result against the
+    oracle.  Every key of the block is visible to every row, so the oracle's
+    offset attention over the sampled rows alone is exact."""
+    up = _upipe()
+    w = W.WORKLOADS["llama8b_ring"]
+    Sq, Skv, Hq, Hkv = w.S, w.extra["kv_len"], w.Hq, w.Hkv
+    qo, ko = w.extra["q_offset"], w.extra["kv_offset"]
+    assert qo - ko >= Skv - 1
+    q, k, v = W.inputs_for(w)
+    qd, kd, vd = q.to(DEV), k.to(DEV), v.to(DEV)
+    outs = {}
+    for U in w.U_sweep:
+        print(f"llama8b_ring Sq={Sq} Skv={Skv} U={U}", flush=True)
+        o, lse = up.attn_fwd_ring(qd, kd, vd, qo, ko, causal=True, U=U)
+        torch.cuda.synchronize()
+        outs[U] = (o, lse)
+    o1, l1 = outs[w.U_sweep[0]]
+    for U in w.U_sweep[1:]:
+        assert torch.equal(outs[U][0].view(torch.int16), o1.view(torch.int16)), U
+        assert torch.equal(outs[U][1].view(torch.int32), l1.view(torch.int32)), U
+    rows = W.sample_rows(Sq, 128, w.seed)
+    print("oracle sampled rows", flush=True)
+    o_r, lse_r = R.attn_fwd_offset(as64(q[rows]), as64(k), as64(v), qo - ko)
+    o_c, l_c = o1.cpu(), l1.cpu()
+    assert_close("o rows", o_c[rows], o_r)
+    _check_lse("lse rows", l_c[:, rows], lse_r)
+    # merged into the block's own causal part (keys = the block's first
+    # Hkv query heads, as in bench.py's running result)
+    kself = q[:, :Hkv].contiguous()
+    ksd = kself.to(DEV)
+    o_acc, lse_acc = up.attn_fwd_ring(qd, ksd, ksd, qo, qo, causal=True, U=1)
+    up.lse_merge(o_acc, lse_acc, o1, l1)
+    torch.cuda.synchronize()
+    o_own, lse_own = A.attn_rows_at(as64(q[rows]), np.asarray(rows), as64(kself), as64(kself),
+                                    causal=True)
+    o_m, lse_m = R.lse_merge(o_own, lse_own, o_r, lse_r)
+    assert_close("merged o rows", o_acc.cpu()[rows], o_m)
+    _check_lse("merged lse rows", lse_acc.cpu()[:, rows], lse_m)
