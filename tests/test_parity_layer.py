@@ -91,8 +91,8 @@ def test_layer_llama_width_short_sequence():
 @pytest.mark.timeout(900)
 def test_llama8b_layer_share_sampled():
     """The Llama3-8B layer share (S = 256K, d_model = 4096, RoPE with Llama 3's
-    base): bitwise equal across U; sampled rows and the key tail against the
-    oracle."""
+    base): bitwise equal across U and between kept and recomputed attention
+    output; sampled rows and the key tail against the oracle."""
     w = W.WORKLOADS["llama8b_layer"]
     S, dm, Hq, Hkv, d = w.S, w.d_model, w.Hq, w.Hkv, w.d
     base = w.extra.get("rope_base")
@@ -104,6 +104,16 @@ def test_llama8b_layer_share_sampled():
     for U in w.U_sweep[1:]:
         for name, a, b in zip(NAMES, outs[1], outs[U]):
             assert _bits_equal(a, b), f"{name}: U=1 vs U={U}"
+    # full checkpointing (attention output recomputed in the backward), as
+    # bench.py --checkpointing full times it: bitwise the kept-output result
+    print(f"llama8b_layer S={S} U=1 full checkpointing", flush=True)
+    up = _upipe()
+    xd, wd, wod, dyd = (t.to(DEV) for t in (x, wqkv, wo, dy))
+    full = up.layer_bwd(xd, wd, wod, None, None, dyd, Hq, Hkv, U=1, rope_base=base or 0.0)
+    torch.cuda.synchronize()
+    for name, a, b in zip(("dx", "dwqkv", "dwo"), outs[1][3:], full):
+        assert _bits_equal(a, b.cpu()), f"{name}: kept vs recomputed output"
+    del xd, wd, wod, dyd, full
     y, o, lse, dx, dwqkv, dwo = outs[1]
     x64, w64, wo64, dy64 = (as64(t) for t in (x, wqkv, wo, dy))
     rows = W.sample_rows(S, 128, w.seed)
