@@ -57,13 +57,18 @@ def parse():
     return p.parse_args()
 
 
-def kernel_flops(S, U, d, causal=True):
-    """Algorithmic flops per launch of each attention kernel (one chunk)."""
+def kernel_flops(S, Hq, B, d, fwd_passes=1, causal=True):
+    """Algorithmic flops per step of each attention kernel family, over all
+    Hq heads of B sequences (independent of how the library splits the heads
+    into launches; per launch it is this over the launch count when the
+    launches are equal).  fwd_passes = 2 when the backward recomputes the
+    forward (full checkpointing)."""
     pairs = S * (S + 1) // 2 if causal else S * S
+    heads = Hq * B
     return {
-        "attn_fwd": 4 * d * U * pairs,          # Q K^T and P V
-        "attn_bwd_dkdv": 8 * d * U * pairs,     # S, dP recompute + dV, dK
-        "attn_bwd_dq": 2 * d * U * pairs,       # dQ (S, dP recomputed again)
+        "attn_fwd": 4 * d * pairs * heads * fwd_passes,   # Q K^T and P V
+        "attn_bwd_dkdv": 8 * d * pairs * heads,           # S, dP recompute + dV, dK
+        "attn_bwd_dq": 2 * d * pairs * heads,             # dQ (S, dP recomputed again)
     }
 
 
@@ -255,7 +260,8 @@ def main():
     ms_per_step = elapsed / args.steps * 1e3
     value = step_flops / (elapsed / args.steps) / 1e12
 
-    kflops = kernel_flops(S, U, d)
+    full_ckpt = w.is_layer and args.checkpointing == "full"
+    kflops = kernel_flops(S, Hq, B, d, fwd_passes=2 if full_ckpt else 1)
     kernels = {}
     for name in upipe.upipe_profile_names():
         n, ms = upipe.upipe_profile_query(name)
@@ -265,7 +271,7 @@ def main():
                  "ms_per_step": round(ms / args.steps, 4),
                  "avg_launch_ms": round(ms / n, 4)}
         if name in kflops:
-            entry["tflops"] = round(kflops[name] / (ms / n / 1e3) / 1e12, 2)
+            entry["tflops"] = round(kflops[name] / (ms / args.steps / 1e3) / 1e12, 2)
         kernels[name] = entry
     dom = max(kernels, key=lambda n: kernels[n]["ms_per_step"])
     achieved = kernels[dom].get("tflops")

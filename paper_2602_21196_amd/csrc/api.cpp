@@ -149,6 +149,26 @@ AttnBwdPlan plan_attn_bwd(int64_t S, int Hq, int Hkv, int U) {
 }
 
 // ------------------------------------------------------- attention paths
+int run_dkdv_chunk(const bf16* Qc, const bf16* dOc, const float* lse_c, const float* D,
+                   const bf16* Kp, const bf16* Vp, float* dK32, float* dV32, bf16* dk, bf16* dv,
+                   int64_t kv_row, int64_t kv_head, int64_t S, int64_t Sp, int U, int h0, int G,
+                   int causal, hipStream_t st) {
+  const bool per_head = U > 1 && (dK32 != nullptr || G == 1);
+  if (!per_head) {
+    UPIPE_LAUNCH(kAttnBwdDkdv, st,
+                 launch_attn_bwd_dkdv(Qc, dOc, lse_c, D, Kp, Vp, dK32, dV32, dk, dv, kv_row,
+                                      kv_head, S, Sp, U, h0, G, causal, st));
+    return UPIPE_OK;
+  }
+  const int64_t head = Sp * HEAD_DIM;
+  for (int u = 0; u < U; ++u)
+    UPIPE_LAUNCH(kAttnBwdDkdv, st,
+                 launch_attn_bwd_dkdv(Qc + u * head, dOc + u * head, lse_c + u * Sp, D + u * Sp,
+                                      Kp, Vp, dK32, dV32, dk, dv, kv_row, kv_head, S, Sp, 1,
+                                      h0 + u, G, causal, st));
+  return UPIPE_OK;
+}
+
 int run_attn_fwd_ring(const bf16* q, const bf16* k, const bf16* v, bf16* o, float* lse,
                       int64_t Sq, int64_t Skv, int64_t delta, int Hq, int Hkv, int causal,
                       int U, char* ws, hipStream_t st) {
@@ -226,10 +246,10 @@ int run_attn_bwd(const bf16* q, const bf16* k, const bf16* v, const bf16* o,
                  launch_rowdot_lse(dout + h0 * HEAD_DIM, (int64_t)Hq * HEAD_DIM, HEAD_DIM,
                                    o + h0 * HEAD_DIM, (int64_t)Hq * HEAD_DIM, HEAD_DIM, lse, S,
                                    h0, U, p.Sp, D, lse_c, st));
-    UPIPE_LAUNCH(kAttnBwdDkdv, st,
-                 launch_attn_bwd_dkdv(Qc, dOc, lse_c, D, Kp, Vp, dK32, dV32, dk, dv,
-                                      (int64_t)Hkv * HEAD_DIM, HEAD_DIM, S, p.Sp, U, h0, G,
-                                      causal, st));
+    const int rc = run_dkdv_chunk(Qc, dOc, lse_c, D, Kp, Vp, dK32, dV32, dk, dv,
+                                  (int64_t)Hkv * HEAD_DIM, HEAD_DIM, S, p.Sp, U, h0, G, causal,
+                                  st);
+    if (rc != UPIPE_OK) return rc;
     UPIPE_LAUNCH(kAttnBwdDq, st,
                  launch_attn_bwd_dq(Qc, dOc, lse_c, D, Kp, Vp, dQc, S, p.Sp, U, h0, G, causal,
                                     RopeArgs{}, st));

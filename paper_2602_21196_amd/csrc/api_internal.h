@@ -84,6 +84,19 @@ struct AttnBwdPlan {
   size_t total = 0;
 };
 
+// dK/dV of the chunk of U heads starting at h0 (arguments as for
+// launch_attn_bwd_dkdv; Qc, dOc, lse_c, D hold the chunk's U heads).  When
+// the fp32 carries exist (dK32 != nullptr: some group spans chunks) or every
+// group is one head (G == 1), the heads go one launch each: the same
+// additions in the same order as a single launch over the chunk (the carries
+// hand each head's sums to the next), but every workgroup of a launch then
+// walks one head's query tiles alongside the others and they share L2
+// lines, where in one launch over several heads they drift apart.
+int run_dkdv_chunk(const bf16* Qc, const bf16* dOc, const float* lse_c, const float* D,
+                   const bf16* Kp, const bf16* Vp, float* dK32, float* dV32, bf16* dk, bf16* dv,
+                   int64_t kv_row, int64_t kv_head, int64_t S, int64_t Sp, int U, int h0, int G,
+                   int causal, hipStream_t st);
+
 AttnFwdPlan plan_attn_fwd(int64_t S, int Hq, int Hkv, int U);
 AttnFwdPlan plan_attn_fwd_ring(int64_t Sq, int64_t Skv, int Hq, int Hkv, int U);
 AttnBwdPlan plan_attn_bwd(int64_t S, int Hq, int Hkv, int U);

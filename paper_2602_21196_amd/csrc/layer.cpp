@@ -285,9 +285,9 @@ int run_layer_bwd_seq(const bf16* x, const bf16* wqkv, const bf16* wo, const bf1
                    launch_rowdot_lse(dOc, HEAD_DIM, head, o_saved + (int64_t)h0 * HEAD_DIM, qw,
                                      HEAD_DIM, lse, S, h0, U, Sp, D, lse_c, st));
     }
-    UPIPE_LAUNCH(kAttnBwdDkdv, st,
-                 launch_attn_bwd_dkdv(Qc, dOc, lse_c, D, Kp, Vp, dK32, dV32, dKh, dVh, HEAD_DIM,
-                                      head, S, Sp, U, h0, G, 1, st));
+    rc = run_dkdv_chunk(Qc, dOc, lse_c, D, Kp, Vp, dK32, dV32, dKh, dVh, HEAD_DIM, head, S, Sp,
+                        U, h0, G, 1, st);
+    if (rc != UPIPE_OK) return rc;
     UPIPE_LAUNCH(kAttnBwdDq, st,
                  launch_attn_bwd_dq(Qc, dOc, lse_c, D, Kp, Vp, dQc, S, Sp, U, h0, G, 1, rope, st));
   }
