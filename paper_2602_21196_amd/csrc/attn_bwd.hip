@@ -51,13 +51,22 @@ struct QStageSrc {
 // This wave's share of one tile's copies: KV_BLK blocks of 1 KB each of Q and
 // dO rows; lanes of wave 0 copy the QT lse values, lanes of wave 1 the QT D
 // values (16 bytes per lane).
-__device__ __forceinline__ void issue_qstage(const QStageSrc& r, const uint32_t (&offr)[KV_BLK],
-                                             uint32_t qb, char* buf, int w, int lane) {
+__device__ __forceinline__ void issue_qstage(const QStageSrc& r, uint32_t qb, char* buf, int w,
+                                             int lane) {
+  // The source offsets are recomputed for every tile (a few VALU
+  // instructions) instead of being held in registers across the tile loop,
+  // where the register file is full; the empty asm keeps the compiler from
+  // hoisting them back out of the loop.
+  asm volatile("" : "+v"(lane));
 #pragma unroll
   for (int i = 0; i < KV_BLK; ++i) {
     const int blk = KV_BLK * w + i;
-    dma_buf_b128(r.q, offr[i], qb * 256u, buf + OFF_Q + blk * 1024);
-    dma_buf_b128(r.dO, offr[i], qb * 256u, buf + OFF_DO + blk * 1024);
+    // this lane's 16 bytes: Q / dO row `row` of the tile (16 lanes per row),
+    // chunk swizzled for the transposing reads
+    const int row = 4 * blk + (lane >> 4);
+    const uint32_t off = row * 256u + (((lane & 15) ^ tsw(row)) << 4);
+    dma_buf_b128(r.q, off, qb * 256u, buf + OFF_Q + blk * 1024);
+    dma_buf_b128(r.dO, off, qb * 256u, buf + OFF_DO + blk * 1024);
   }
   if (lane < QT / 4) {
     if (w == 0) dma_buf_b128(r.lse, lane * 16u, qb * 4u, buf + OFF_LSE);
@@ -131,15 +140,22 @@ __device__ __forceinline__ void subtile_pds(const f32x16& sacc, const f32x16& pa
 #pragma unroll
     for (int b = 0; b < 4; ++b) p[4 * a + b] = fast_exp2(fmaf(sacc[4 * a + b], kSl2, -l4[b]));
   }
-  if (CAUSAL && diag) {   // wave-uniform: only tiles that cross the diagonal
-#pragma unroll
-    for (int i = 0; i < 16; ++i)
-      if (mykey > qs + 8 * (i >> 2) + 4 * g + (i & 3)) p[i] = 0.f;
-  }
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
     pf[i >> 3][i & 7] = (bf16)p[i];
     sf[i >> 3][i & 7] = (bf16)(p[i] * pacc[i]);
+  }
+  // Tiles across the diagonal (wave-uniform): zero the entries of keys after
+  // the row, by selection (unmasked they may be inf or NaN).  Done after the
+  // conversions, so that the branch closes the region instead of splitting
+  // its MFMA / VALU interleave in two.
+  if (CAUSAL && diag) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      if (mykey > qs + 8 * (i >> 2) + 4 * g + (i & 3)) {
+        pf[i >> 3][i & 7] = (bf16)0.f;
+        sf[i >> 3][i & 7] = (bf16)0.f;
+      }
   }
 }
 
@@ -231,13 +247,6 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(
   const uint32_t per_head = nqt - qt_lo;
   const int total = (int)(per_head * (hhi - hlo));
 
-  uint32_t offr[KV_BLK];
-#pragma unroll
-  for (int i = 0; i < KV_BLK; ++i) {
-    const int blk = KV_BLK * w + i;
-    const int r = 4 * blk + (lane >> 4);      // Q / dO row of the tile, 16 lanes per row
-    offr[i] = r * 256u + (((lane & 15) ^ tsw(r)) << 4);
-  }
   auto srcs = [&](int hh) {
     QStageSrc r;
     const int64_t hoff = (int64_t)(hh - h0) * Sp * HEAD_DIM;
@@ -250,7 +259,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(
 
   // First tile: head hlo, query tile nqt-1.
   QStageSrc cur = srcs(hlo);
-  issue_qstage(cur, offr, (nqt - 1) * QT, smem, w, lane);
+  issue_qstage(cur, (nqt - 1) * QT, smem, w, lane);
 
   // K and -V B-operand fragments (lane = key column, k = head dim); -V makes
   // the dP products count down from D.
@@ -262,6 +271,14 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(
     for (int s = 0; s < 8; ++s) {
       kf[s] = *reinterpret_cast<const bf16x8*>(kp + 16 * s);
       vf[s] = -*reinterpret_cast<const bf16x8*>(vp + 16 * s);
+    }
+    // They are only ever MFMA operands, which may come from AGPRs: placing
+    // them there leaves the VGPRs to the score accumulators and the P / dS
+    // arithmetic (fewer AGPR -> VGPR moves, no spills).
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      asm volatile("" : "+a"(kf[s]));
+      asm volatile("" : "+a"(vf[s]));
     }
   }
 
@@ -305,7 +322,7 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(
     __syncthreads();   // this tile landed for all waves; the other buffer is free
     if (it + 1 < total) {
       if (nh != hh) cur = srcs(nh);
-      issue_qstage(cur, offr, nq * QT, smem + ((it + 1) & 1) * KV_STAGE, w, lane);
+      issue_qstage(cur, nq * QT, smem + ((it + 1) & 1) * KV_STAGE, w, lane);
     }
     // Pairs of 32-row subtiles, upper rows first; a pair is needed when its
     // last row reaches this wave's first key (and lies inside the sequence).
