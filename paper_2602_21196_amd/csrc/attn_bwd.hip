@@ -192,19 +192,20 @@ __device__ __forceinline__ void interleave_mfma_valu() {
 //   B: S/dP products of the lower subtile   | P, dS of the upper subtile
 //   C: dV/dK products of the upper subtile  | P, dS of the lower subtile
 //   D: dV/dK products of the lower subtile
-// The LDS fragments of each block are read one region ahead.  The lower
-// subtile is computed even where only the upper one is needed: the diagonal
-// mask then zeroes all of its P and dS.
-template <bool CAUSAL>
+// The LDS fragments of each block are read one region ahead; fa holds the
+// upper subtile's S / dP fragments on entry, and with PF it is refilled
+// during region D (which has no other LDS reads) with those of the next
+// pair of the tile.  The lower subtile is computed even where only the upper
+// one is needed: the diagonal mask then zeroes all of its P and dS.
+template <bool CAUSAL, bool PF>
 __device__ __forceinline__ void pair_step(const char* buf, int base, uint32_t qb, uint32_t kw,
                                           uint32_t mykey, int r32, int g, int lane,
                                           const bf16x8 (&kf)[8], const bf16x8 (&vf)[8],
-                                          f32x16 (&dva)[4], f32x16 (&dka)[4]) {
-  Frags fa, fb;
+                                          f32x16 (&dva)[4], f32x16 (&dka)[4], Frags& fa) {
+  Frags fb;
   f32x16 s1, p1, s0, p0;
   bf16x8 pf1[2], sf1[2], pf0[2], sf0[2];
   const uint32_t q1 = qb + base + 32, q0 = qb + base;
-  read_sdp(buf, base + 32, r32, g, fa);
   read_sdp(buf, base, r32, g, fb);
   __builtin_amdgcn_sched_barrier(0);
   subtile_sdp(fa, kf, vf, buf, base + 32, g, s1, p1);                                            // A
@@ -212,14 +213,15 @@ __device__ __forceinline__ void pair_step(const char* buf, int base, uint32_t qb
   __builtin_amdgcn_sched_barrier(0);
   subtile_sdp(fb, kf, vf, buf, base, g, s0, p0);                                            // B
   subtile_pds<CAUSAL>(s1, p1, buf, base + 32, q1, mykey, q1 < kw + 31, g, pf1, sf1);
-  read_dvdk(buf, base, lane, fb);
   interleave_mfma_valu();
   __builtin_amdgcn_sched_barrier(0);
   dvdk_products(fa, pf1, sf1, dva, dka);                                      // C
+  read_dvdk(buf, base, lane, fb);
   subtile_pds<CAUSAL>(s0, p0, buf, base, q0, mykey, q0 < kw + 31, g, pf0, sf0);
   interleave_mfma_valu();
   __builtin_amdgcn_sched_barrier(0);
   dvdk_products(fb, pf0, sf0, dva, dka);                                      // D
+  if (PF) read_sdp(buf, base - 32, r32, g, fa);   // the next pair's upper subtile
 }
 
 template <bool CAUSAL>
@@ -326,11 +328,17 @@ __global__ __launch_bounds__(256, 1) void attn_bwd_dkdv_kernel(
     }
     // Pairs of 32-row subtiles, upper rows first; a pair is needed when its
     // last row reaches this wave's first key (and lies inside the sequence).
-#pragma unroll
-    for (int pp = QT / 64 - 1; pp >= 0; --pp) {
-      const uint32_t pb = qb + 64 * pp;
-      if (pb < Spv && (!CAUSAL || pb + 63 >= kw))
-        pair_step<CAUSAL>(buf, 64 * pp, qb, kw, mykey, r32, g, lane, kf, vf, dva, dka);
+    // The upper pair reads the lower pair's first fragments in its region D.
+    Frags fa;
+    const bool run1 = qb + 64 < Spv && (!CAUSAL || qb + 127 >= kw);
+    const bool run0 = qb < Spv && (!CAUSAL || qb + 63 >= kw);
+    if (run1) {
+      read_sdp(buf, 96, r32, g, fa);
+      pair_step<CAUSAL, true>(buf, 64, qb, kw, mykey, r32, g, lane, kf, vf, dva, dka, fa);
+    }
+    if (run0) {
+      if (!run1) read_sdp(buf, 32, r32, g, fa);
+      pair_step<CAUSAL, false>(buf, 0, qb, kw, mykey, r32, g, lane, kf, vf, dva, dka, fa);
     }
     qt = nq;
     hh = nh;
