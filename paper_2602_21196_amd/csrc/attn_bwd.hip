@@ -124,14 +124,12 @@ __device__ __forceinline__ void subtile_sdp(const Frags& fr, const bf16x8 (&kf)[
   }
 }
 
-// P and -dS of one subtile (rows `sub`.. of the tile, first row qs) as bf16 A
-// operands, from its scores, the staged lse rows and D - dP.  Negation is
-// exact and commutes with rounding, so the dK accumulators carry exactly -dK
-// (the final scale is -1/sqrt d).
-template <bool CAUSAL>
+// P and -dS of one subtile (rows `sub`.. of the tile) as bf16 A operands,
+// from its scores, the staged lse rows and D - dP.  Negation is exact and
+// commutes with rounding, so the dK accumulators carry exactly -dK (the
+// final scale is -1/sqrt d).  No masking here (subtile_mask).
 __device__ __forceinline__ void subtile_pds(const f32x16& sacc, const f32x16& pacc, const char* buf,
-                                            int sub, uint32_t qs, uint32_t mykey, bool diag, int g,
-                                            bf16x8 (&pf)[2], bf16x8 (&sf)[2]) {
+                                            int sub, int g, bf16x8 (&pf)[2], bf16x8 (&sf)[2]) {
   const float* lsel = reinterpret_cast<const float*>(buf + OFF_LSE) + sub;
   float p[16];
 #pragma unroll
@@ -145,10 +143,16 @@ __device__ __forceinline__ void subtile_pds(const f32x16& sacc, const f32x16& pa
     pf[i >> 3][i & 7] = (bf16)p[i];
     sf[i >> 3][i & 7] = (bf16)(p[i] * pacc[i]);
   }
-  // Tiles across the diagonal (wave-uniform): zero the entries of keys after
-  // the row, by selection (unmasked they may be inf or NaN).  Done after the
-  // conversions, so that the branch closes the region instead of splitting
-  // its MFMA / VALU interleave in two.
+}
+
+// Subtiles across the diagonal (wave-uniform `diag`; first row qs): zero the
+// P and dS entries of keys after the row, by selection (unmasked they may be
+// inf or NaN).  This runs after the conversions and between two regions: a
+// branch ends the compiler's scheduling block, and inside a region it would
+// split the MFMA / VALU interleave in two.
+template <bool CAUSAL>
+__device__ __forceinline__ void subtile_mask(uint32_t qs, uint32_t mykey, bool diag, int g,
+                                             bf16x8 (&pf)[2], bf16x8 (&sf)[2]) {
   if (CAUSAL && diag) {
 #pragma unroll
     for (int i = 0; i < 16; ++i)
@@ -212,14 +216,16 @@ __device__ __forceinline__ void pair_step(const char* buf, int base, uint32_t qb
   read_dvdk(buf, base + 32, lane, fa);
   __builtin_amdgcn_sched_barrier(0);
   subtile_sdp(fb, kf, vf, buf, base, g, s0, p0);                                            // B
-  subtile_pds<CAUSAL>(s1, p1, buf, base + 32, q1, mykey, q1 < kw + 31, g, pf1, sf1);
+  subtile_pds(s1, p1, buf, base + 32, g, pf1, sf1);
   interleave_mfma_valu();
   __builtin_amdgcn_sched_barrier(0);
+  subtile_mask<CAUSAL>(q1, mykey, q1 < kw + 31, g, pf1, sf1);
   dvdk_products(fa, pf1, sf1, dva, dka);                                      // C
   read_dvdk(buf, base, lane, fb);
-  subtile_pds<CAUSAL>(s0, p0, buf, base, q0, mykey, q0 < kw + 31, g, pf0, sf0);
+  subtile_pds(s0, p0, buf, base, g, pf0, sf0);
   interleave_mfma_valu();
   __builtin_amdgcn_sched_barrier(0);
+  subtile_mask<CAUSAL>(q0, mykey, q0 < kw + 31, g, pf0, sf0);
   dvdk_products(fb, pf0, sf0, dva, dka);                                      // D
   if (PF) read_sdp(buf, base - 32, r32, g, fa);   // the next pair's upper subtile
 }
