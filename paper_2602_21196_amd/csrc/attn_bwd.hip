@@ -176,12 +176,12 @@ __device__ __forceinline__ void dvdk_products(const Frags& fr, const bf16x8 (&pf
 }
 
 // Scheduling request for a region of 16 MFMAs and the VALU work of one
-// subtile's P and dS: its LDS reads first, then one MFMA after every few VALU
-// instructions, so the matrix unit and the vector ALU of the one wave on the
-// SIMD work side by side.
+// subtile's P and dS: one MFMA after every few VALU instructions, so the
+// matrix unit and the vector ALU of the one wave on the SIMD work side by
+// side (the region's LDS reads are left to the scheduler: asking for them
+// first bunched the first MFMAs behind them).
 constexpr int KV_NV = 5;   // VALU instructions requested between two MFMAs
 __device__ __forceinline__ void interleave_mfma_valu() {
-  __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
