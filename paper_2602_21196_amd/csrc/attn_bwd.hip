@@ -181,6 +181,17 @@ __device__ __forceinline__ void dvdk_products(const Frags& fr, const bf16x8 (&pf
 // side (the region's LDS reads are left to the scheduler: asking for them
 // first bunched the first MFMAs behind them).
 constexpr int KV_NV = 5;   // VALU instructions requested between two MFMAs
+// Region A (no VALU): its 16 MFMAs with the 32 transposing reads of the
+// next block's fragments, two per MFMA; region D with the next pair's
+// fragment reads, one per MFMA.
+template <int NDS>
+__device__ __forceinline__ void interleave_mfma_lds() {
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, NDS, 0);
+  }
+}
 __device__ __forceinline__ void interleave_mfma_valu() {
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
@@ -214,6 +225,7 @@ __device__ __forceinline__ void pair_step(const char* buf, int base, uint32_t qb
   __builtin_amdgcn_sched_barrier(0);
   subtile_sdp(fa, kf, vf, buf, base + 32, g, s1, p1);                                            // A
   read_dvdk(buf, base + 32, lane, fa);
+  interleave_mfma_lds<2>();
   __builtin_amdgcn_sched_barrier(0);
   subtile_sdp(fb, kf, vf, buf, base, g, s0, p0);                                            // B
   subtile_pds(s1, p1, buf, base + 32, g, pf1, sf1);
@@ -227,7 +239,10 @@ __device__ __forceinline__ void pair_step(const char* buf, int base, uint32_t qb
   __builtin_amdgcn_sched_barrier(0);
   subtile_mask<CAUSAL>(q0, mykey, q0 < kw + 31, g, pf0, sf0);
   dvdk_products(fb, pf0, sf0, dva, dka);                                      // D
-  if (PF) read_sdp(buf, base - 32, r32, g, fa);   // the next pair's upper subtile
+  if (PF) {   // the next pair's upper subtile
+    read_sdp(buf, base - 32, r32, g, fa);
+    interleave_mfma_lds<1>();
+  }
 }
 
 template <bool CAUSAL>
