@@ -73,6 +73,9 @@ SHAPES = [
     (200, 4, 4, True),
     (257, 2, 1, False),
     (96, 4, 2, False),
+    (2500, 4, 2, False),    # many tiles, ragged tail; the forward splits its key range
+    (4100, 8, 2, True),     # U = 2: carried per-head dK/dV; U = 4: one group per launch;
+                            # U = 8: two groups per launch
 ]
 
 
