@@ -166,12 +166,15 @@ def cpu_baseline(w, q, k, v, do, target_s):
 
 def workspace_model_gb(S, Hq, Hkv, d, U):
     """Attention-only backward workspace model A + B U (the larger of the two
-    workspaces): resident packed K, V (+ fp32 dK, dV carries when a key/value
-    group spans chunks) and, per chunk head, Q, dO, dQ (bf16) and lse, D."""
+    workspaces): resident packed K, V (none when one key/value head of a
+    length that is a multiple of 128 is read in place), fp32 dK, dV carries
+    when a key/value group spans chunks, and, per chunk head, Q, dO, dQ
+    (bf16) and lse, D."""
     Sp = (S + 127) // 128 * 128
     G = Hq // Hkv   # a group spans chunks when its first and last heads differ in h // U
     carry = any((g * G) // U != ((g + 1) * G - 1) // U for g in range(Hkv))
-    fixed = 2 * Sp * Hkv * d * 2 + (2 * Sp * Hkv * d * 4 if carry else 0)
+    packed_kv = not (Hkv == 1 and S % 128 == 0)
+    fixed = (2 * Sp * Hkv * d * 2 if packed_kv else 0) + (2 * Sp * Hkv * d * 4 if carry else 0)
     return (fixed + U * Sp * (3 * d * 2 + 2 * 4)) / 1e9
 
 

@@ -40,8 +40,8 @@
  *    next synchronisation.  No C++ exception crosses this interface.
  *  - Supported shapes: d == 128; S >= 1 (any length: rows past the last tile
  *    are padded inside the workspace); 1 <= Hkv <= Hq, Hkv | Hq; 1 <= U,
- *    U | Hq; Hq <= 64; S * max(Hq, d_model/128) * d < 2^40.  A batch of B
- *    sequences needs B >= 1 and B times one sequence's largest tensor below
+ *    U | Hq; Hq <= 64; S * max(Hq, d_model/128) * d < 2^40.  The batched
+ *    calls need B >= 1 and B times one sequence's largest tensor below
  *    2^61 elements (UPIPE_ERR_INVALID_ARG otherwise).
  *  - Thread safety: calls are reentrant across host threads and streams as
  *    long as each concurrent call has its own workspace and outputs.  The
@@ -99,7 +99,8 @@ int upipe_gqa_schedule(int H, int Hkv, int C, int U, int* stage_heads,
  * needs for these shapes, or 0 if the shapes are invalid or unsupported.
  * The size is  fixed(S, Hkv[, d_model]) + U * per_head(S)  (chunk buffers).
  * It does not depend on the batch size B: the calls that take a batch of B
- * sequences run them one after another through the same workspace.
+ * sequences run them one after another through the same workspace.  The
+ * attention calls keep no key/value copy when Hkv == 1 and S % 128 == 0.
  * ---------------------------------------------------------------------- */
 size_t upipe_attn_fwd_workspace_size(int64_t S, int Hq, int Hkv, int d, int U);
 size_t upipe_attn_bwd_workspace_size(int64_t S, int Hq, int Hkv, int d, int U);
@@ -110,23 +111,33 @@ size_t upipe_layer_bwd_workspace_size(int64_t S, int d_model, int Hq, int Hkv,
 
 /* ------------------------------------------------------------------------
  * Attention forward, head chunk by head chunk (Section 2.1 definition,
- * Section 3.3 chunking, Appendix A "Untied Ulysses (forward)"), for a batch
- * of B independent sequences of length S (B >= 1; the paper's batch-size
- * ablation spends the memory UPipe saves on B > 1).
+ * Section 3.3 chunking, Appendix A "Untied Ulysses (forward)").
  *
- *   q   bf16 [B, S, Hq, d]   queries, token-major (the Ulysses layout)
- *   k   bf16 [B, S, Hkv, d]  keys
- *   v   bf16 [B, S, Hkv, d]  values
- *   o   bf16 [B, S, Hq, d]   out: softmax(q k^T / sqrt d) v per head
- *   lse fp32 [B, Hq, S]      out: natural-log log-sum-exp of each row's
- *                            scaled scores (saved for the backward)
+ *   q   bf16 [S, Hq, d]    queries, token-major (the Ulysses layout)
+ *   k   bf16 [S, Hkv, d]   keys
+ *   v   bf16 [S, Hkv, d]   values
+ *   o   bf16 [S, Hq, d]    out: softmax(q k^T / sqrt d) v per head
+ *   lse fp32 [Hq, S]       out: natural-log log-sum-exp of each row's scaled
+ *                          scores (saved for the backward)
  * For each chunk c the U heads [cU, (c+1)U) are packed to a head-major chunk
  * buffer (the stand-in for the input all-to-all's destination), attended, and
- * unpacked into o (the output all-to-all's target, `final_out`).
+ * unpacked into o (the output all-to-all's target, `final_out`).  With one
+ * key/value head and S a multiple of 128, k and v already have the
+ * head-major layout and are read in place (no copy in the workspace).
  * ---------------------------------------------------------------------- */
 int upipe_attn_fwd(const void* q, const void* k, const void* v, void* o,
-                   float* lse, int64_t B, int64_t S, int Hq, int Hkv, int d, int causal,
+                   float* lse, int64_t S, int Hq, int Hkv, int d, int causal,
                    int U, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* The same for a batch of B >= 1 independent sequences of length S (the
+ * paper's batch-size ablation, Appendix "Batch Size Ablation", spends the
+ * memory UPipe saves on B > 1): q, o [B, S, Hq, d], k, v [B, S, Hkv, d],
+ * lse [B, Hq, S].  The sequences run one after another through the same
+ * workspace, whose size does not depend on B.  B = 1 is upipe_attn_fwd. */
+int upipe_attn_fwd_batch(const void* q, const void* k, const void* v, void* o,
+                         float* lse, int64_t B, int64_t S, int Hq, int Hkv, int d,
+                         int causal, int U, void* ws, size_t ws_bytes,
+                         hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * One ring step of context-parallel attention (Section 2.2, Ring Attention
@@ -174,18 +185,27 @@ int upipe_lse_merge(void* o, float* lse, const void* o_part, const float* lse_pa
  * Appendix A "Untied Ulysses (backward)": per-stage dQ, per-group dK/dV
  * accumulators that persist across stages).
  *
- *   q, k, v, o, lse  as produced/consumed by upipe_attn_fwd (same B, S)
- *   dout bf16 [B, S, Hq, d]   upstream gradient of o
- *   dq   bf16 [B, S, Hq, d]   out
- *   dk   bf16 [B, S, Hkv, d]  out: summed over each group's query heads
- *   dv   bf16 [B, S, Hkv, d]  out
+ *   q, k, v, o, lse  as produced/consumed by upipe_attn_fwd (same S)
+ *   dout bf16 [S, Hq, d]   upstream gradient of o
+ *   dq   bf16 [S, Hq, d]   out
+ *   dk   bf16 [S, Hkv, d]  out: summed over each group's query heads
+ *   dv   bf16 [S, Hkv, d]  out
  * `lse` must come from upipe_attn_fwd on the same q, k, v (it is used to
  * rebuild the probabilities without a second softmax pass).
  * ---------------------------------------------------------------------- */
 int upipe_attn_bwd(const void* q, const void* k, const void* v, const void* o,
                    const float* lse, const void* dout, void* dq, void* dk,
-                   void* dv, int64_t B, int64_t S, int Hq, int Hkv, int d, int causal,
+                   void* dv, int64_t S, int Hq, int Hkv, int d, int causal,
                    int U, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* The same for a batch of B >= 1 sequences (Appendix "Batch Size
+ * Ablation"), layouts as for upipe_attn_fwd_batch with dout, dq like q and
+ * dk, dv like k.  B = 1 is upipe_attn_bwd. */
+int upipe_attn_bwd_batch(const void* q, const void* k, const void* v, const void* o,
+                         const float* lse, const void* dout, void* dq, void* dk,
+                         void* dv, int64_t B, int64_t S, int Hq, int Hkv, int d,
+                         int causal, int U, void* ws, size_t ws_bytes,
+                         hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * Rotary position embedding (RoFormer), in place (Section 4 "Implementation":
@@ -208,27 +228,21 @@ int upipe_rope(void* x, int64_t S, int H, int d, int64_t pos0, double base, int 
  * Attention block forward (Section 3.3, Appendix A "Untied Ulysses
  * (forward)": per stage, QKV projection of the stage's heads, attention,
  * output written into its slot of `final_out`; after the last stage the
- * output projection y = final_out wo).  Always causal.  A batch of B >= 1
- * independent sequences of length S; every sequence starts at position pos0.
+ * output projection y = final_out wo).  Always causal.
  *
- *   x         bf16 [B, S, d_model]               hidden states
+ *   x         bf16 [S, d_model]                  hidden states
  *   wqkv      bf16 [d_model, (Hq + 2 Hkv) d]     columns [Q heads|K|V]
  *   wo        bf16 [Hq d, d_model]               output projection
- *   y         bf16 [B, S, d_model]               out: final_out @ wo
- *   o_saved   bf16 [B, S, Hq, d]                 out: final_out (attention
+ *   y         bf16 [S, d_model]                  out: final_out @ wo
+ *   o_saved   bf16 [S, Hq, d]                    out: final_out (attention
  *                                                output, saved for backward)
- *   lse_saved fp32 [B, Hq, S]                    out: row log-sum-exp
- *   rope_base  0: no rotary embedding; > 0: Q and K heads are rotated as by
- *              upipe_rope(base = rope_base, pos0) inside the projection,
- *              before their single rounding to bf16 (Section 4
- *              "Implementation": in place, no fp32 copy, no extra pass)
- *   pos0       position of row 0 (same limits as upipe_rope)
+ *   lse_saved fp32 [Hq, S]                       out: row log-sum-exp
  * d_model must be a multiple of 128.
  * ---------------------------------------------------------------------- */
 int upipe_layer_fwd(const void* x, const void* wqkv, const void* wo, void* y,
-                    void* o_saved, float* lse_saved, int64_t B, int64_t S, int d_model,
-                    int Hq, int Hkv, int d, int U, double rope_base, int64_t pos0,
-                    void* ws, size_t ws_bytes, hipStream_t stream);
+                    void* o_saved, float* lse_saved, int64_t S, int d_model,
+                    int Hq, int Hkv, int d, int U, void* ws, size_t ws_bytes,
+                    hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * Attention block backward (Appendix A "Untied Ulysses (backward)"): the
@@ -239,31 +253,54 @@ int upipe_layer_fwd(const void* x, const void* wqkv, const void* wo, void* y,
  * one product.  K and V are recomputed from x (activation checkpointing
  * keeps only x, final_out, lse).
  *
- *   x, wqkv, wo, B     as for upipe_layer_fwd
- *   rope_base, pos0    as for upipe_layer_fwd (the same values): Q and K are
- *                      recomputed rotated, and the gradients of the rotated
- *                      Q and K are turned back by the inverse rotation
- *                      before the projection gradients use them
+ *   x, wqkv, wo        as for upipe_layer_fwd
  *   o_saved, lse_saved the forward's outputs for the same x and weights
  *                      (selective checkpointing: the attention output is
  *                      kept), or both NULL (full checkpointing: each
  *                      chunk's attention forward is recomputed, bitwise
  *                      equal to the forward's, at the cost of one more
  *                      attention forward; the results are identical)
- *   dy    bf16 [B, S, d_model]              upstream gradient of y
- *   dx    bf16 [B, S, d_model]              out
- *   dwqkv bf16 [d_model, (Hq + 2 Hkv) d]    out: summed over the batch
- *   dwo   bf16 [Hq d, d_model]              out: summed over the batch
+ *   dy    bf16 [S, d_model]                 upstream gradient of y
+ *   dx    bf16 [S, d_model]                 out
+ *   dwqkv bf16 [d_model, (Hq + 2 Hkv) d]    out
+ *   dwo   bf16 [Hq d, d_model]              out
  * Weight gradients reduce over S with a fixed split of the sequence and a
- * fixed-order sum of the partial products, then over the batch in sequence
- * order in fp32, rounded once (deterministic, no atomics).
+ * fixed-order sum of the partial products in fp32, rounded once
+ * (deterministic, no atomics).
  * ---------------------------------------------------------------------- */
 int upipe_layer_bwd(const void* x, const void* wqkv, const void* wo,
                     const void* o_saved, const float* lse_saved,
                     const void* dy, void* dx, void* dwqkv, void* dwo,
-                    int64_t B, int64_t S, int d_model, int Hq, int Hkv, int d, int U,
-                    double rope_base, int64_t pos0, void* ws, size_t ws_bytes,
-                    hipStream_t stream);
+                    int64_t S, int d_model, int Hq, int Hkv, int d, int U,
+                    void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * The block with a batch of B >= 1 sequences (Appendix "Batch Size
+ * Ablation") and rotary position embedding of Q and K (Section 4
+ * "Implementation": RoPE applied in place inside the projection, with no
+ * fp32 copy and no extra pass).  x, y, dy, dx [B, S, d_model], o_saved
+ * [B, S, Hq, d], lse_saved [B, Hq, S]; every sequence starts at position
+ * pos0.  dwqkv and dwo are summed over the batch in sequence order in fp32
+ * and rounded once.
+ *   rope_base  0: no rotary embedding; > 0: Q and K heads are rotated as by
+ *              upipe_rope(base = rope_base, pos0) on the fp32 projection
+ *              accumulators before their single rounding to bf16; the
+ *              backward recomputes them rotated and turns the gradients of
+ *              the rotated Q and K back by the inverse rotation
+ *   pos0       position of row 0 (same limits as upipe_rope)
+ * The backward must get the same B, rope_base and pos0 as the forward.
+ * With B = 1, rope_base = 0 these are upipe_layer_fwd / upipe_layer_bwd.
+ * ---------------------------------------------------------------------- */
+int upipe_layer_fwd_ex(const void* x, const void* wqkv, const void* wo, void* y,
+                       void* o_saved, float* lse_saved, int64_t B, int64_t S,
+                       int d_model, int Hq, int Hkv, int d, int U, double rope_base,
+                       int64_t pos0, void* ws, size_t ws_bytes, hipStream_t stream);
+int upipe_layer_bwd_ex(const void* x, const void* wqkv, const void* wo,
+                       const void* o_saved, const float* lse_saved,
+                       const void* dy, void* dx, void* dwqkv, void* dwo,
+                       int64_t B, int64_t S, int d_model, int Hq, int Hkv, int d,
+                       int U, double rope_base, int64_t pos0, void* ws,
+                       size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * Kernel timing (measurement aid).  While enabled, every kernel the library

@@ -313,3 +313,47 @@ def attn_key_tail_at(q_tail, do_tail, k, v, j0):
             dk[:n - j0, g, :] += (ds[:, j0:].T @ q_tail[sl, h, :]) / np.sqrt(d)
             dv[:n - j0, g, :] += p[:, j0:].T @ do_tail[sl, h, :]
     return dk, dv
+
+
+def attn_key_cols_given(q, do, k, v, o, lse, cols, causal=True, row_block=4096):
+    """dK and dV at the listed key columns, given each query row's lse and o.
+
+    The Section 2.1 gradient for key j of key/value head g:
+        dV_j = sum_{h in group g} sum_{i sees j} P_ij dO_i
+        dK_j = sum_{h in group g} sum_{i sees j} P_ij (dO_i.v_j - D_i) q_i / sqrt(d)
+    with P_ij = exp(q_i.k_j / sqrt(d) - lse_i) and D_i = dO_i . o_i.  Unlike
+    ``attn_bwd`` the row statistics lse [Hq, S] and the output o [S, Hq, d]
+    are the caller's: with the oracle's own they give exactly the oracle's
+    gradient; with another implementation's they give that implementation's
+    gradient as it should be for its own statistics ("conditioned" on them),
+    which isolates the error of its key-gradient accumulation.  Only the
+    listed columns are formed, so one column costs O(S Hq d) work at any
+    length.  q, do, o may be any float arrays; rows are taken to float64 in
+    blocks of ``row_block``.  Returns (dk, dv), each [len(cols), Hkv, d].
+    """
+    cols = np.asarray(cols, np.int64)
+    S, Hq, d = q.shape
+    Hkv = k.shape[1]
+    kc = np.asarray(k[cols], np.float64)
+    vc = np.asarray(v[cols], np.float64)
+    lse = np.asarray(lse, np.float64)
+    dk = np.zeros((len(cols), Hkv, d))
+    dv = np.zeros((len(cols), Hkv, d))
+    lo = int(cols.min()) if causal else 0
+    for b0 in range(lo, S, row_block):
+        b1 = min(S, b0 + row_block)
+        r = np.arange(b0, b1)
+        qb = np.asarray(q[b0:b1], np.float64)
+        dob = np.asarray(do[b0:b1], np.float64)
+        ob = np.asarray(o[b0:b1], np.float64)
+        vis = cols[None, :] <= r[:, None] if causal else np.ones((len(r), len(cols)), bool)
+        for h in range(Hq):
+            g = kv_head_of(h, Hq, Hkv)
+            s = (qb[:, h, :] @ kc[:, g, :].T) / np.sqrt(d)
+            p = np.where(vis, np.exp(np.where(vis, s, 0.0) - lse[h, b0:b1][:, None]), 0.0)
+            D = np.sum(dob[:, h, :] * ob[:, h, :], axis=1)
+            dp = dob[:, h, :] @ vc[:, g, :].T
+            ds = p * (dp - D[:, None])
+            dv[:, g, :] += p.T @ dob[:, h, :]
+            dk[:, g, :] += (ds.T @ qb[:, h, :]) / np.sqrt(d)
+    return dk, dv

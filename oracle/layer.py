@@ -107,3 +107,47 @@ def layer_fwd_rows(x, wqkv, wo, Hq, Hkv, d, rows, rope_base=None, pos0=0):
     o, lse = attention.attn_fwd(q, k, v, True, rows=rows)
     y = o.reshape(len(rows), Hq * d) @ wo
     return y, o, lse
+
+
+def layer_bwd_tail(x, wqkv, wo, dy, Hq, Hkv, d, j0, rope_base=None, pos0=0):
+    """dX at the rows [j0, S) of the causal block (same chain rule as
+    ``layer_bwd``).
+
+    Row s of dX = [dQ_s | dK_s | dV_s] wqkv^T.  dQ_s is row-local; under the
+    causal mask dK_s and dV_s receive only from query rows >= s, so the rows
+    [j0, S) need the attention gradient of those query rows alone (each with
+    its full row softmax).  K and V are needed at every position.
+    """
+    x = np.asarray(x, np.float64)
+    wqkv = np.asarray(wqkv, np.float64)
+    wo = np.asarray(wo, np.float64)
+    dy = np.asarray(dy, np.float64)
+    S = x.shape[0]
+    q, k, v = split_qkv(x @ wqkv, Hq, Hkv, d)
+    q = _rotate(q, S, rope_base, pos0)
+    k = _rotate(k, S, rope_base, pos0)
+    do = (dy @ wo.T).reshape(S, Hq, d)
+    tail = np.arange(j0, S)
+    dq, _ = attention.attn_bwd_rows(q, k, v, do, tail)
+    dk, dv = attention.attn_bwd_key_tail(q, k, v, do, j0)
+    if rope_base is not None:
+        dq = rope(dq, pos0 + tail, rope_base, inverse=True)
+        dk = rope(dk, pos0 + tail, rope_base, inverse=True)
+    n = len(tail)
+    dqkv = np.concatenate([dq.reshape(n, -1), dk.reshape(n, -1), dv.reshape(n, -1)], axis=1)
+    return dqkv @ wqkv.T
+
+
+def dwo_given_output(o, dy, cols):
+    """Columns ``cols`` of dWo = final_out^T dY for a given final_out o
+    [S, Hq, d] (the chain rule of y = final_out wo): [Hq d, len(cols)].
+
+    With the oracle's own final_out this is the oracle's dWo; with another
+    implementation's saved output it is the weight gradient that output
+    implies ("conditioned" on it), which checks the reduction over the whole
+    sequence without re-running attention.
+    """
+    o = np.asarray(o, np.float64)
+    S = o.shape[0]
+    dyc = np.asarray(dy[:, cols], np.float64)
+    return o.reshape(S, -1).T @ dyc

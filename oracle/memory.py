@@ -8,7 +8,9 @@ hold one against the other:
 1. The closed forms printed in Tables ``tab:gqa_fwd_mem`` (Section 3.2) and
    ``tab:gqa_bwd_mem`` (Appendix A), in units of one local hidden-state shard
    (S/C * d_model bf16 elements), with gamma = 1 + 2/G the combined size of
-   Q, K, V and nu = H/U the number of stages.
+   Q, K, V and nu = H/U the number of stages.  Only the two rows the tests
+   can hold against something else are kept: UPipe, and Ulysses with
+   offloading, which is what UPipe reduces to at nu = 1.
 2. The live-tensor inventories of the Appendix A paragraphs ("DeepSpeed-
    Ulysses (forward/backward)", "Untied Ulysses (forward/backward)"): which
    tensors are alive at each moment and how large each is.
@@ -45,14 +47,10 @@ def saving_fraction(H, U):
 # columns: before attn block, during inp_all_to_all, during attn kernel,
 #          during out_all_to_all
 
-def fwd_table(method, G, nu=1, L=1, pi=1):
+def fwd_table(method, G, nu=1):
     g = gamma(G)
-    if method == "ulysses":
-        return (F(L), L + (g + 1), L + (g + 1), F(L + 2))
     if method == "ulysses_offload":
         return (F(1), g + 2, g + 2, F(3))
-    if method == "fpdt":
-        return (F(1, pi), (g + 2) / pi, (2 * g + 1) / pi, F(2, pi))
     if method == "upipe":
         return (F(1), 2 + g / nu, 2 + g / nu, 2 + F(1, nu))
     raise ValueError(method)
@@ -62,14 +60,10 @@ def fwd_table(method, G, nu=1, L=1, pi=1):
 # columns: before bwd attn, during out_all_to_all, during bwd attn kernel,
 #          during inp_all_to_all
 
-def bwd_table(method, G, nu=1, L=1, pi=1):
+def bwd_table(method, G, nu=1):
     g = gamma(G)
-    if method == "ulysses":
-        return (F(L + 2), F(L + 3), L + 2 * g + 2, L + g + 1)
     if method == "ulysses_offload":
         return (F(3), F(4), 2 * g + 3, g + 2)
-    if method == "fpdt":
-        return (F(1, pi), F(3, pi), (2 * g + 4) / pi, (g + 2) / pi)
     if method == "upipe":
         kernel = max(3 + 2 * g / nu, 2 + 2 * g / nu + F(2 * (nu - 1), nu))
         return (F(3), 3 + F(1, nu), kernel, 2 + g / nu + F(2 * (nu - 1), nu))

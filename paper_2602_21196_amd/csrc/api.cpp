@@ -112,8 +112,11 @@ AttnFwdPlan plan_attn_fwd_ring(int64_t Sq, int64_t Skv, int Hq, int Hkv, int U) 
   p.Skvp = round_up(Skv, SEQ_PAD);
   const size_t qhead = (size_t)p.Sp * HEAD_DIM * 2, kvhead = (size_t)p.Skvp * HEAD_DIM * 2;
   Carver c;
-  p.Kp = c.take(Hkv * kvhead);
-  p.Vp = c.take(Hkv * kvhead);
+  p.kv_direct = kv_in_place(Skv, Hkv);
+  if (!p.kv_direct) {
+    p.Kp = c.take(Hkv * kvhead);
+    p.Vp = c.take(Hkv * kvhead);
+  }
   p.Qc = c.take(U * qhead);
   p.ns = attn_fwd_key_splits(p.Sp, p.Skvp);
   p.Oc = c.take(p.ns * U * qhead);
@@ -132,8 +135,11 @@ AttnBwdPlan plan_attn_bwd(int64_t S, int Hq, int Hkv, int U) {
   const size_t head = (size_t)p.Sp * HEAD_DIM * 2;
   const size_t row32 = (size_t)p.Sp * 4;
   Carver c;
-  p.Kp = c.take(Hkv * head);
-  p.Vp = c.take(Hkv * head);
+  p.kv_direct = kv_in_place(S, Hkv);
+  if (!p.kv_direct) {
+    p.Kp = c.take(Hkv * head);
+    p.Vp = c.take(Hkv * head);
+  }
   p.carry = group_split(Hq, Hkv, U);
   if (p.carry) {
     p.dK32 = c.take(Hkv * head * 2);
@@ -173,16 +179,20 @@ int run_attn_fwd_ring(const bf16* q, const bf16* k, const bf16* v, bf16* o, floa
                       int64_t Sq, int64_t Skv, int64_t delta, int Hq, int Hkv, int causal,
                       int U, char* ws, hipStream_t st) {
   const AttnFwdPlan p = plan_attn_fwd_ring(Sq, Skv, Hq, Hkv, U);
-  bf16* Kp = (bf16*)(ws + p.Kp);
-  bf16* Vp = (bf16*)(ws + p.Vp);
+  const bf16* Kp = p.kv_direct ? k : (const bf16*)(ws + p.Kp);
+  const bf16* Vp = p.kv_direct ? v : (const bf16*)(ws + p.Vp);
   bf16* Qc = (bf16*)(ws + p.Qc);
   bf16* Oc = (bf16*)(ws + p.Oc);
   const int G = Hq / Hkv;
-  // Key/value heads: packed once, resident for every chunk (on one device
-  // the GQA schedule needs each key/value head from its group's first stage
-  // on, Section 4.1).
-  UPIPE_LAUNCH(kPackRows, st, launch_pack_rows(k, Skv, Hkv, 0, Hkv, p.Skvp, Kp, st));
-  UPIPE_LAUNCH(kPackRows, st, launch_pack_rows(v, Skv, Hkv, 0, Hkv, p.Skvp, Vp, st));
+  // Key/value heads: packed once (unless already head-major), resident for
+  // every chunk (on one device the GQA schedule needs each key/value head
+  // from its group's first stage on, Section 4.1).
+  if (!p.kv_direct) {
+    UPIPE_LAUNCH(kPackRows, st,
+                 launch_pack_rows(k, Skv, Hkv, 0, Hkv, p.Skvp, (bf16*)(ws + p.Kp), st));
+    UPIPE_LAUNCH(kPackRows, st,
+                 launch_pack_rows(v, Skv, Hkv, 0, Hkv, p.Skvp, (bf16*)(ws + p.Vp), st));
+  }
   for (int h0 = 0; h0 < Hq; h0 += U) {
     UPIPE_LAUNCH(kPackRows, st, launch_pack_rows(q, Sq, Hq, h0, U, p.Sp, Qc, st));
     if (p.ns == 1) {
@@ -227,8 +237,8 @@ int run_attn_bwd(const bf16* q, const bf16* k, const bf16* v, const bf16* o,
                  bf16* dv, int64_t S, int Hq, int Hkv, int causal, int U,
                  char* ws, hipStream_t st) {
   const AttnBwdPlan p = plan_attn_bwd(S, Hq, Hkv, U);
-  bf16* Kp = (bf16*)(ws + p.Kp);
-  bf16* Vp = (bf16*)(ws + p.Vp);
+  const bf16* Kp = p.kv_direct ? k : (const bf16*)(ws + p.Kp);
+  const bf16* Vp = p.kv_direct ? v : (const bf16*)(ws + p.Vp);
   float* dK32 = p.carry ? (float*)(ws + p.dK32) : nullptr;
   float* dV32 = p.carry ? (float*)(ws + p.dV32) : nullptr;
   bf16* Qc = (bf16*)(ws + p.Qc);
@@ -237,8 +247,12 @@ int run_attn_bwd(const bf16* q, const bf16* k, const bf16* v, const bf16* o,
   float* D = (float*)(ws + p.D);
   float* lse_c = (float*)(ws + p.lse_c);
   const int G = Hq / Hkv;
-  UPIPE_LAUNCH(kPackRows, st, launch_pack_rows(k, S, Hkv, 0, Hkv, p.Sp, Kp, st));
-  UPIPE_LAUNCH(kPackRows, st, launch_pack_rows(v, S, Hkv, 0, Hkv, p.Sp, Vp, st));
+  if (!p.kv_direct) {
+    UPIPE_LAUNCH(kPackRows, st,
+                 launch_pack_rows(k, S, Hkv, 0, Hkv, p.Sp, (bf16*)(ws + p.Kp), st));
+    UPIPE_LAUNCH(kPackRows, st,
+                 launch_pack_rows(v, S, Hkv, 0, Hkv, p.Sp, (bf16*)(ws + p.Vp), st));
+  }
   for (int h0 = 0; h0 < Hq; h0 += U) {
     UPIPE_LAUNCH(kPackRows, st, launch_pack_rows(q, S, Hq, h0, U, p.Sp, Qc, st));
     UPIPE_LAUNCH(kPackRows, st, launch_pack_rows(dout, S, Hq, h0, U, p.Sp, dOc, st));
@@ -305,9 +319,9 @@ size_t upipe_attn_bwd_workspace_size(int64_t S, int Hq, int Hkv, int d, int U) {
   return plan_attn_bwd(S, Hq, Hkv, U).total;
 }
 
-int upipe_attn_fwd(const void* q, const void* k, const void* v, void* o,
-                   float* lse, int64_t B, int64_t S, int Hq, int Hkv, int d, int causal,
-                   int U, void* ws, size_t ws_bytes, hipStream_t stream) {
+static int attn_fwd_batch(const void* q, const void* k, const void* v, void* o, float* lse,
+                          int64_t B, int64_t S, int Hq, int Hkv, int d, int causal, int U,
+                          void* ws, size_t ws_bytes, hipStream_t stream) {
   try {
     int rc = check_attn_shape(S, Hq, Hkv, d, U);
     if (rc != UPIPE_OK) return rc;
@@ -329,6 +343,18 @@ int upipe_attn_fwd(const void* q, const void* k, const void* v, void* o,
   } catch (...) {
     return UPIPE_ERR_HIP;
   }
+}
+
+int upipe_attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, int64_t S,
+                   int Hq, int Hkv, int d, int causal, int U, void* ws, size_t ws_bytes,
+                   hipStream_t stream) {
+  return attn_fwd_batch(q, k, v, o, lse, 1, S, Hq, Hkv, d, causal, U, ws, ws_bytes, stream);
+}
+
+int upipe_attn_fwd_batch(const void* q, const void* k, const void* v, void* o, float* lse,
+                         int64_t B, int64_t S, int Hq, int Hkv, int d, int causal, int U,
+                         void* ws, size_t ws_bytes, hipStream_t stream) {
+  return attn_fwd_batch(q, k, v, o, lse, B, S, Hq, Hkv, d, causal, U, ws, ws_bytes, stream);
 }
 
 size_t upipe_attn_fwd_ring_workspace_size(int64_t Sq, int64_t Skv, int Hq, int Hkv, int d, int U) {
@@ -399,10 +425,10 @@ int upipe_rope(void* x, int64_t S, int H, int d, int64_t pos0, double base, int 
   }
 }
 
-int upipe_attn_bwd(const void* q, const void* k, const void* v, const void* o,
-                   const float* lse, const void* dout, void* dq, void* dk,
-                   void* dv, int64_t B, int64_t S, int Hq, int Hkv, int d, int causal,
-                   int U, void* ws, size_t ws_bytes, hipStream_t stream) {
+static int attn_bwd_batch(const void* q, const void* k, const void* v, const void* o,
+                          const float* lse, const void* dout, void* dq, void* dk, void* dv,
+                          int64_t B, int64_t S, int Hq, int Hkv, int d, int causal, int U,
+                          void* ws, size_t ws_bytes, hipStream_t stream) {
   try {
     int rc = check_attn_shape(S, Hq, Hkv, d, U);
     if (rc != UPIPE_OK) return rc;
@@ -425,6 +451,21 @@ int upipe_attn_bwd(const void* q, const void* k, const void* v, const void* o,
   } catch (...) {
     return UPIPE_ERR_HIP;
   }
+}
+
+int upipe_attn_bwd(const void* q, const void* k, const void* v, const void* o, const float* lse,
+                   const void* dout, void* dq, void* dk, void* dv, int64_t S, int Hq, int Hkv,
+                   int d, int causal, int U, void* ws, size_t ws_bytes, hipStream_t stream) {
+  return attn_bwd_batch(q, k, v, o, lse, dout, dq, dk, dv, 1, S, Hq, Hkv, d, causal, U, ws,
+                        ws_bytes, stream);
+}
+
+int upipe_attn_bwd_batch(const void* q, const void* k, const void* v, const void* o,
+                         const float* lse, const void* dout, void* dq, void* dk, void* dv,
+                         int64_t B, int64_t S, int Hq, int Hkv, int d, int causal, int U,
+                         void* ws, size_t ws_bytes, hipStream_t stream) {
+  return attn_bwd_batch(q, k, v, o, lse, dout, dq, dk, dv, B, S, Hq, Hkv, d, causal, U, ws,
+                        ws_bytes, stream);
 }
 
 int upipe_profile_enable(int on) {

@@ -69,16 +69,23 @@ struct Carver {
   size_t take(size_t bytes);
 };
 
+// Token-major keys/values [S, Hkv, d] already are the head-major [Hkv, Sp, d]
+// the kernels read when there is one key/value head and no padding: then they
+// are read in place instead of being copied into the workspace.
+inline bool kv_in_place(int64_t S, int Hkv) { return Hkv == 1 && S % SEQ_PAD == 0; }
+
 struct AttnFwdPlan {
   int64_t Sp = 0;     // query rows, padded
   int64_t Skvp = 0;   // key/value rows, padded
   int ns = 1;         // key splits per query block (their partial results are merged)
+  bool kv_direct = false;   // keys/values read in place (no Kp, Vp)
   size_t Kp = 0, Vp = 0, Qc = 0, Oc = 0, lse_part = 0, total = 0;
 };
 
 struct AttnBwdPlan {
   int64_t Sp = 0;
   bool carry = false;  // a key/value group spans several chunks
+  bool kv_direct = false;   // keys/values read in place (no Kp, Vp)
   size_t Kp = 0, Vp = 0, dK32 = 0, dV32 = 0;
   size_t Qc = 0, dOc = 0, dQc = 0, D = 0, lse_c = 0;
   size_t total = 0;

@@ -352,10 +352,10 @@ size_t upipe_layer_bwd_workspace_size(int64_t S, int d_model, int Hq, int Hkv, i
   return plan_layer_bwd(S, d_model, Hq, Hkv, U).total;
 }
 
-int upipe_layer_fwd(const void* x, const void* wqkv, const void* wo, void* y, void* o_saved,
-                    float* lse_saved, int64_t B, int64_t S, int d_model, int Hq, int Hkv, int d,
-                    int U, double rope_base, int64_t pos0, void* ws, size_t ws_bytes,
-                    hipStream_t stream) {
+int upipe_layer_fwd_ex(const void* x, const void* wqkv, const void* wo, void* y, void* o_saved,
+                       float* lse_saved, int64_t B, int64_t S, int d_model, int Hq, int Hkv,
+                       int d, int U, double rope_base, int64_t pos0, void* ws,
+                       size_t ws_bytes, hipStream_t stream) {
   try {
     int rc = check_layer_shape(S, d_model, Hq, Hkv, d, U);
     if (rc != UPIPE_OK) return rc;
@@ -376,11 +376,11 @@ int upipe_layer_fwd(const void* x, const void* wqkv, const void* wo, void* y, vo
   }
 }
 
-int upipe_layer_bwd(const void* x, const void* wqkv, const void* wo, const void* o_saved,
-                    const float* lse_saved, const void* dy, void* dx, void* dwqkv, void* dwo,
-                    int64_t B, int64_t S, int d_model, int Hq, int Hkv, int d, int U,
-                    double rope_base, int64_t pos0, void* ws, size_t ws_bytes,
-                    hipStream_t stream) {
+int upipe_layer_bwd_ex(const void* x, const void* wqkv, const void* wo, const void* o_saved,
+                       const float* lse_saved, const void* dy, void* dx, void* dwqkv,
+                       void* dwo, int64_t B, int64_t S, int d_model, int Hq, int Hkv, int d,
+                       int U, double rope_base, int64_t pos0, void* ws, size_t ws_bytes,
+                       hipStream_t stream) {
   try {
     int rc = check_layer_shape(S, d_model, Hq, Hkv, d, U);
     if (rc != UPIPE_OK) return rc;
@@ -405,6 +405,21 @@ int upipe_layer_bwd(const void* x, const void* wqkv, const void* wo, const void*
   } catch (...) {
     return UPIPE_ERR_HIP;
   }
+}
+
+int upipe_layer_fwd(const void* x, const void* wqkv, const void* wo, void* y, void* o_saved,
+                    float* lse_saved, int64_t S, int d_model, int Hq, int Hkv, int d, int U,
+                    void* ws, size_t ws_bytes, hipStream_t stream) {
+  return upipe_layer_fwd_ex(x, wqkv, wo, y, o_saved, lse_saved, 1, S, d_model, Hq, Hkv, d, U,
+                            0.0, 0, ws, ws_bytes, stream);
+}
+
+int upipe_layer_bwd(const void* x, const void* wqkv, const void* wo, const void* o_saved,
+                    const float* lse_saved, const void* dy, void* dx, void* dwqkv, void* dwo,
+                    int64_t S, int d_model, int Hq, int Hkv, int d, int U, void* ws,
+                    size_t ws_bytes, hipStream_t stream) {
+  return upipe_layer_bwd_ex(x, wqkv, wo, o_saved, lse_saved, dy, dx, dwqkv, dwo, 1, S, d_model,
+                            Hq, Hkv, d, U, 0.0, 0, ws, ws_bytes, stream);
 }
 
 }  // extern "C"

@@ -40,19 +40,70 @@ def test_status_strings_and_version():
 FAKE = 1 << 20   # a 16-byte aligned non-null address; never dereferenced
 
 
+def _call(plain, batch, a, kw):
+    """The contract call without B; with B in kw, only the batched call.
+    Without B both run and must agree (B = 1 is the contract call)."""
+    a.update(kw)
+    if "B" in kw:
+        return batch(*a.values())
+    b = a.pop("B")
+    r = plain(*a.values())
+    a["B"] = b
+    order = list(a)   # B sits before S in the batched signature
+    args = [a[n] for n in order[:order.index("S")] if n != "B"] + [1] + \
+        [a[n] for n in order[order.index("S"):] if n != "B"]
+    assert batch(*args) == r
+    return r
+
+
 def _fwd(**kw):
     a = dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=FAKE, B=1, S=512, Hq=4, Hkv=1,
              d=128, causal=1, U=1, ws=FAKE, ws_bytes=1 << 40, stream=None)
-    a.update(kw)
-    return upipe.upipe_attn_fwd(*a.values())
+    return _call(upipe.upipe_attn_fwd, upipe.upipe_attn_fwd_batch, a, kw)
 
 
 def _bwd(**kw):
     a = dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=FAKE, dout=FAKE, dq=FAKE,
              dk=FAKE, dv=FAKE, B=1, S=512, Hq=4, Hkv=1, d=128, causal=1, U=1,
              ws=FAKE, ws_bytes=1 << 40, stream=None)
-    a.update(kw)
-    return upipe.upipe_attn_bwd(*a.values())
+    return _call(upipe.upipe_attn_bwd, upipe.upipe_attn_bwd_batch, a, kw)
+
+
+# The four compute calls of the boundary, parameter by parameter.
+CONTRACT = {
+    "upipe_attn_fwd": ["const void*"] * 3 + ["void*", "float*", "int64_t"] + ["int"] * 5 +
+                      ["void*", "size_t", "hipStream_t"],
+    "upipe_attn_bwd": ["const void*"] * 4 + ["const float*", "const void*"] + ["void*"] * 3 +
+                      ["int64_t"] + ["int"] * 5 + ["void*", "size_t", "hipStream_t"],
+    "upipe_layer_fwd": ["const void*"] * 3 + ["void*", "void*", "float*", "int64_t"] +
+                       ["int"] * 5 + ["void*", "size_t", "hipStream_t"],
+    "upipe_layer_bwd": ["const void*"] * 4 + ["const float*", "const void*"] + ["void*"] * 3 +
+                       ["int64_t"] + ["int"] * 5 + ["void*", "size_t", "hipStream_t"],
+}
+_CTYPE = {"const void*": ctypes.c_void_p, "void*": ctypes.c_void_p,
+          "float*": ctypes.c_void_p, "const float*": ctypes.c_void_p,
+          "int64_t": ctypes.c_int64, "int": ctypes.c_int, "size_t": ctypes.c_size_t,
+          "hipStream_t": ctypes.c_void_p}
+
+
+def _prototype(name):
+    src = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    m = re.search(r"\bint\s+" + name + r"\s*\(([^)]*)\)", src)
+    assert m, name
+    types = []
+    for par in m.group(1).split(","):
+        par = " ".join(par.split())
+        par = re.sub(r"\s*\*\s*", "* ", par).strip()
+        types.append(par.rsplit(" ", 1)[0].replace("* ", "*").strip())
+    return types
+
+
+@pytest.mark.parametrize("name", sorted(CONTRACT))
+def test_contract_signatures(name):
+    """upipe_attn_fwd / upipe_attn_bwd / upipe_layer_fwd / upipe_layer_bwd take
+    exactly the contract's parameters, in the header and in the binding."""
+    assert _prototype(name) == CONTRACT[name]
+    assert upipe._SIGNATURES[name][1] == [_CTYPE[t] for t in CONTRACT[name]]
 
 
 @pytest.mark.parametrize("fn", [_fwd, _bwd])
@@ -108,11 +159,16 @@ def test_ring_step_validation_and_workspace():
     # the key range is split in two, with a second O buffer and fp32 lse rows
     # for both halves.
     qh, kh = 512 * 128 * 2, 384 * 128 * 2
+    # One key/value head and 384 = 3 x 128 keys: K, V are read in place.
     for U in (1, 2, 4):
         assert upipe.upipe_attn_fwd_ring_workspace_size(512, 384, 4, 1, 128, U) == \
-            2 * kh + U * qh + 2 * U * qh + 2 * U * 512 * 4
+            U * qh + 2 * U * qh + 2 * U * 512 * 4
+        assert upipe.upipe_attn_fwd_ring_workspace_size(512, 384, 4, 2, 128, U) == \
+            2 * 2 * kh + U * qh + 2 * U * qh + 2 * U * 512 * 4
     # a single key stage: no split
-    assert upipe.upipe_attn_fwd_ring_workspace_size(512, 128, 4, 1, 128, 1) == \
+    assert upipe.upipe_attn_fwd_ring_workspace_size(512, 128, 4, 1, 128, 1) == 2 * qh
+    # a ragged key length is packed (padded) once
+    assert upipe.upipe_attn_fwd_ring_workspace_size(512, 100, 4, 1, 128, 1) == \
         2 * 128 * 256 + 2 * qh
     # equal lengths: the plain forward's workspace
     assert upipe.upipe_attn_fwd_ring_workspace_size(1000, 1000, 4, 2, 128, 2) == \
@@ -135,19 +191,25 @@ def test_workspace_sizes_follow_the_plan():
     Sp = S
     head = Sp * d * 2
     for U in (1, 2, 4):
+        # one key/value head, S a multiple of 128: K and V read in place
         fwd = upipe.upipe_attn_fwd_workspace_size(S, 4, 1, d, U)
-        assert fwd == 2 * head + 2 * U * head
+        assert fwd == 2 * U * head
         bwd = upipe.upipe_attn_bwd_workspace_size(S, 4, 1, d, U)
         carry = 4 * head if U < 4 else 0          # fp32 dK, dV accumulators
-        # K, V resident; per chunk head Q, dO, dQ and the fp32 D and lse rows
-        assert bwd == 2 * head + carry + 3 * U * head + 2 * U * Sp * 4
+        # per chunk head Q, dO, dQ and the fp32 D and lse rows
+        assert bwd == carry + 3 * U * head + 2 * U * Sp * 4
+        # two key/value heads: K, V packed once and resident
+        assert upipe.upipe_attn_fwd_workspace_size(S, 4, 2, d, U) == 4 * head + 2 * U * head
+        carry2 = 8 * head if U < 2 else 0
+        assert upipe.upipe_attn_bwd_workspace_size(S, 4, 2, d, U) == \
+            4 * head + carry2 + 3 * U * head + 2 * U * Sp * 4
     # padding of a ragged length to the 128-row granule (one key stage: no split)
     assert upipe.upipe_attn_fwd_workspace_size(1, 1, 1, d, 1) == 4 * 128 * d * 2
     # 32768 rows = 128 query blocks of 256: keys split in two; one row more
     # makes 129 blocks: no split
     s32 = 32768 * d * 2
     assert upipe.upipe_attn_fwd_workspace_size(32768, 4, 1, d, 1) == \
-        2 * s32 + s32 + 2 * s32 + 2 * 32768 * 4
+        s32 + 2 * s32 + 2 * 32768 * 4
     s33 = 32896 * d * 2
     assert upipe.upipe_attn_fwd_workspace_size(32769, 4, 1, d, 1) == 2 * s33 + 2 * s33
     assert upipe.upipe_attn_fwd_workspace_size(0, 1, 1, d, 1) == 0
@@ -185,22 +247,28 @@ def test_layer_entry_points_validate():
     S, dm = 256, 512
     assert upipe.upipe_layer_fwd_workspace_size(S, 500, 4, 1, 128, 1) == 0
     assert upipe.upipe_layer_fwd_workspace_size(S, dm, 4, 1, 64, 1) == 0
-    assert upipe.upipe_layer_fwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, S, dm, 4,
-                                 1, 128, 3, 0.0, 0, FAKE, 1 << 40, None) == -1
-    assert upipe.upipe_layer_fwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0, S, dm, 4,
-                                 1, 128, 1, 0.0, 0, FAKE, 1 << 40, None) == -1   # B = 0
+    assert upipe.upipe_layer_fwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, S, dm, 4,
+                                 1, 128, 3, FAKE, 1 << 40, None) == -1
+    assert upipe.upipe_layer_fwd_ex(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, S, dm, 4,
+                                    1, 128, 3, 0.0, 0, FAKE, 1 << 40, None) == -1
+    assert upipe.upipe_layer_fwd_ex(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0, S, dm, 4,
+                                    1, 128, 1, 0.0, 0, FAKE, 1 << 40, None) == -1   # B = 0
+    assert upipe.upipe_layer_fwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, S, dm, 4,
+                                 1, 128, 1, FAKE, 1024, None) == -3
+    assert upipe.upipe_layer_bwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, S, dm,
+                                 4, 1, 128, 1, FAKE, 1024, None) == -3
 
 
 def _layer(fn, **kw):
     a = dict(B=1, S=256, dm=512, Hq=4, Hkv=1, d=128, U=1, base=5e5, pos0=0)
     a.update(kw)
     if fn == "fwd":
-        return upipe.upipe_layer_fwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, a["B"], a["S"],
-                                     a["dm"], a["Hq"], a["Hkv"], a["d"], a["U"], a["base"],
-                                     a["pos0"], FAKE, 0, None)
-    return upipe.upipe_layer_bwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
-                                 a["B"], a["S"], a["dm"], a["Hq"], a["Hkv"], a["d"], a["U"],
-                                 a["base"], a["pos0"], FAKE, 0, None)
+        return upipe.upipe_layer_fwd_ex(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, a["B"], a["S"],
+                                        a["dm"], a["Hq"], a["Hkv"], a["d"], a["U"], a["base"],
+                                        a["pos0"], FAKE, 0, None)
+    return upipe.upipe_layer_bwd_ex(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                    a["B"], a["S"], a["dm"], a["Hq"], a["Hkv"], a["d"], a["U"],
+                                    a["base"], a["pos0"], FAKE, 0, None)
 
 
 @pytest.mark.parametrize("fn", ["fwd", "bwd"])
@@ -228,8 +296,11 @@ def test_layer_bwd_saved_output_both_or_neither():
     S, dm = 256, 512
 
     def bwd(o, lse):
-        return upipe.upipe_layer_bwd(FAKE, FAKE, FAKE, o, lse, FAKE, FAKE, FAKE, FAKE, 1, S, dm,
-                                     4, 1, 128, 1, 0.0, 0, FAKE, 0, None)
+        r = upipe.upipe_layer_bwd(FAKE, FAKE, FAKE, o, lse, FAKE, FAKE, FAKE, FAKE, S, dm,
+                                  4, 1, 128, 1, FAKE, 0, None)
+        assert upipe.upipe_layer_bwd_ex(FAKE, FAKE, FAKE, o, lse, FAKE, FAKE, FAKE, FAKE, 1, S,
+                                        dm, 4, 1, 128, 1, 0.0, 0, FAKE, 0, None) == r
+        return r
     assert bwd(FAKE, FAKE) == WS           # kept output (selective checkpointing)
     assert bwd(None, None) == WS           # recomputed (full checkpointing)
     assert bwd(FAKE, None) == INV
@@ -251,3 +322,49 @@ def test_rope_entry_point_validates():
     assert r(FAKE, 16, 4, 128, -5, 1e4, 0, None) == UNS
     assert r(FAKE, 16, 4, 128, (1 << 32) - 15, 1e4, 0, None) == UNS
     assert r(FAKE, 16, 65, 128, 0, 1e4, 0, None) == UNS
+
+
+def _cpu(*shape):
+    import torch
+    return torch.zeros(shape, dtype=torch.bfloat16)
+
+
+def test_torch_wrappers_check_every_shape():
+    """The binding checks each tensor's full shape before the library sees a
+    raw pointer (a mismatch would be read or written out of bounds on the
+    GPU); these CPU tensors never reach a device."""
+    import torch
+    S, Hq, Hkv, d = 256, 4, 1, 128
+    q, k = _cpu(S, Hq, d), _cpu(S, Hkv, d)
+    lse = torch.zeros((Hq, S))
+    bad = [
+        lambda: upipe.attn_fwd(q, _cpu(S, Hkv, 64), k),
+        lambda: upipe.attn_fwd(q, k, _cpu(S + 1, Hkv, d)),
+        lambda: upipe.attn_fwd(q, _cpu(1, S, Hkv, d), k),
+        lambda: upipe.attn_fwd(_cpu(2, S, Hq, d), _cpu(2, S, Hkv, d), _cpu(1, S, Hkv, d)),
+        lambda: upipe.attn_bwd(q, k, k, _cpu(S, Hq - 1, d), lse, q),
+        lambda: upipe.attn_bwd(q, k, k, q, torch.zeros((Hq, S - 1)), q),
+        lambda: upipe.attn_bwd(q, k, k, q, lse, _cpu(S, Hq, d + 8)),
+        lambda: upipe.attn_fwd_ring(q, k, _cpu(S, 2, d), 0, 0),
+        lambda: upipe.lse_merge(q, lse, _cpu(S, Hq, d), torch.zeros((Hq, S + 1))),
+        lambda: upipe.rope(_cpu(S, d), 1e4),
+    ]
+    dm = 512
+    x, wqkv, wo = _cpu(S, dm), _cpu(dm, (Hq + 2 * Hkv) * d), _cpu(Hq * d, dm)
+    bad += [
+        lambda: upipe.layer_fwd(x, _cpu(dm, (Hq + 1) * d), wo, Hq, Hkv),
+        lambda: upipe.layer_fwd(x, wqkv, _cpu(Hq * d, dm + 128), Hq, Hkv),
+        lambda: upipe.layer_fwd(x, wqkv, wo, Hq, 2),
+        lambda: upipe.layer_bwd(x, wqkv, wo, _cpu(S, Hq, d), lse, _cpu(S, dm - 1), Hq, Hkv),
+        lambda: upipe.layer_bwd(x, wqkv, wo, _cpu(S, Hq, 64), lse, x, Hq, Hkv),
+        lambda: upipe.layer_bwd(x, wqkv, wo, _cpu(S, Hq, d), torch.zeros((Hq + 1, S)), x,
+                                Hq, Hkv),
+    ]
+    for i, call in enumerate(bad):
+        with pytest.raises(ValueError, match="shape|must be|lse_merge"):
+            call()
+    # right shapes get as far as the device check
+    with pytest.raises(ValueError, match="GPU"):
+        upipe.attn_fwd(q, k, k)
+    with pytest.raises(ValueError, match="GPU"):
+        upipe.layer_bwd(x, wqkv, wo, _cpu(S, Hq, d), lse, x, Hq, Hkv)

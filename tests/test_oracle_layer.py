@@ -51,3 +51,44 @@ def test_layer_rows_match_full():
     np.testing.assert_allclose(yr, y[rows], atol=1e-12)
     np.testing.assert_allclose(orow, o[rows], atol=1e-12)
     np.testing.assert_allclose(lr, lse[:, rows], atol=1e-12)
+
+
+def _layer_inputs(seed, S, dm, Hq, Hkv, d):
+    rng = np.random.default_rng(seed)
+    return (rng.standard_normal((S, dm)), rng.standard_normal((dm, (Hq + 2 * Hkv) * d)) * 0.3,
+            rng.standard_normal((Hq * d, dm)) * 0.3, rng.standard_normal((S, dm)))
+
+
+def test_layer_bwd_tail_matches_torch_autograd():
+    """dX on the last rows from the tail chain rule equals torch float64
+    autograd's dX there (no rotary embedding)."""
+    S, dm, Hq, Hkv, d = 60, 20, 4, 2, 6
+    x, wqkv, wo, dy = _layer_inputs(11, S, dm, Hq, Hkv, d)
+    _, dx_t, _, _ = _torch_layer(x, wqkv, wo, dy, Hq, Hkv, d)
+    for j0 in (0, 1, 37, 59):
+        got = L.layer_bwd_tail(x, wqkv, wo, dy, Hq, Hkv, d, j0)
+        np.testing.assert_allclose(got, dx_t[j0:], rtol=0, atol=1e-10)
+
+
+def test_layer_bwd_tail_with_rope_matches_full_backward():
+    S, dm, Hq, Hkv, d = 50, 16, 2, 1, 8
+    x, wqkv, wo, dy = _layer_inputs(12, S, dm, Hq, Hkv, d)
+    dx, _, _ = L.layer_bwd(x, wqkv, wo, dy, Hq, Hkv, d, rope_base=100.0, pos0=7)
+    got = L.layer_bwd_tail(x, wqkv, wo, dy, Hq, Hkv, d, 30, rope_base=100.0, pos0=7)
+    np.testing.assert_allclose(got, dx[30:], rtol=0, atol=1e-11)
+    # a global position shift changes nothing (scores depend on i - j only),
+    # a different base does
+    same = L.layer_bwd_tail(x, wqkv, wo, dy, Hq, Hkv, d, 30, rope_base=100.0, pos0=8)
+    np.testing.assert_allclose(same, dx[30:], rtol=0, atol=1e-11)
+    bad = L.layer_bwd_tail(x, wqkv, wo, dy, Hq, Hkv, d, 30, rope_base=50.0, pos0=7)
+    assert np.abs(bad - dx[30:]).max() > 1e-3
+
+
+def test_dwo_given_output_matches_torch_autograd():
+    S, dm, Hq, Hkv, d = 45, 24, 4, 2, 6
+    x, wqkv, wo, dy = _layer_inputs(13, S, dm, Hq, Hkv, d)
+    _, _, _, dwo_t = _torch_layer(x, wqkv, wo, dy, Hq, Hkv, d)
+    _, o, _ = L.layer_fwd(x, wqkv, wo, Hq, Hkv, d)
+    cols = np.array([0, 5, 23])
+    np.testing.assert_allclose(L.dwo_given_output(o, dy, cols), dwo_t[:, cols], rtol=0,
+                               atol=1e-10)

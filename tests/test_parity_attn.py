@@ -144,6 +144,15 @@ def test_llama8b_share_sampled_rows_and_invariants():
     dk_t, dv_t = A.attn_bwd_key_tail(q64, k64, v64, do64, j0)
     assert_close("dk tail", dk[j0:], dk_t)
     assert_close("dv tail", dv[j0:], dv_t)
+    # Interior keys (the longest fp32 chains, key 0 gathers from every row):
+    # dK_j, dV_j in float64 from the definition, conditioned on the GPU's lse
+    # and on D = dO.O from the GPU's O.
+    cols = W.sample_key_cols(S, 64, w.seed)
+    print(f"oracle: {len(cols)} key columns conditioned on the GPU's lse and O", flush=True)
+    dk_c, dv_c = A.attn_key_cols_given(q.float().numpy(), do.float().numpy(), k64, v64,
+                                       o.float().numpy(), lse.numpy(), cols)
+    assert_close("dk cols (conditioned on GPU lse, D)", dk[cols], dk_c)
+    assert_close("dv cols (conditioned on GPU lse)", dv[cols], dv_c)
     # Whole-tensor invariants: sum_j dK_j = 0, sum_j dV_j = sum_i dO_i.
     dk64, dv64 = as64(dk), as64(dv)
     col_scale = np.sqrt(S) * np.sqrt(np.mean(dk64 ** 2, axis=0))

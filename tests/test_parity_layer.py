@@ -6,9 +6,7 @@ import pytest
 import torch
 
 import workloads as W
-from oracle import attention as A
 from oracle import layer as L
-from oracle import rope as R
 from tol import as64, assert_close
 
 pytestmark = pytest.mark.gpu
@@ -125,21 +123,15 @@ def test_llama8b_layer_share_sampled():
     # dX on the last rows: dq rows are row-local, dk/dv of the key tail need
     # only the query rows at or after it.
     j0 = S - 256
-    print("oracle key tail", flush=True)
-    q, k, v = L.split_qkv(x64 @ w64, Hq, Hkv, d)
-    tail = np.arange(j0, S)
-    if base is not None:   # attention sees rotated Q, K; their gradients turn back
-        q = R.rope(q, np.arange(S), base)
-        k = R.rope(k, np.arange(S), base)
-    do = (dy64 @ wo64.T).reshape(S, Hq, d)
-    dq_t, _ = A.attn_bwd_rows(q, k, v, do, tail)
-    dk_t, dv_t = A.attn_bwd_key_tail(q, k, v, do, j0)
-    if base is not None:
-        dq_t = R.rope(dq_t, tail, base, inverse=True)
-        dk_t = R.rope(dk_t, tail, base, inverse=True)
-    dqkv = np.concatenate([dq_t.reshape(len(tail), -1), dk_t.reshape(len(tail), -1),
-                           dv_t.reshape(len(tail), -1)], axis=1)
-    assert_close("dx tail rows", dx[j0:], dqkv @ w64.T)
+    print("oracle dx tail", flush=True)
+    assert_close("dx tail rows", dx[j0:],
+                 L.layer_bwd_tail(x64, w64, wo64, dy64, Hq, Hkv, d, j0, rope_base=base))
+    # dWo over the whole sequence (the fixed split-K path with all its pieces),
+    # on sampled columns, conditioned on the GPU's saved attention output.
+    cols = W.sample_key_cols(dm, 64, w.seed)
+    print(f"oracle dwo: {len(cols)} columns conditioned on the GPU's o_saved", flush=True)
+    assert_close("dwo cols (conditioned on GPU o_saved)", dwo[:, cols],
+                 L.dwo_given_output(o.float().numpy(), dy64, cols), rms_scaled=True)
 
 
 @pytest.mark.parametrize("S,dm,Hq,Hkv,base", [(300, 256, 4, 1, 0.0), (513, 384, 4, 2, 5e5),

@@ -1,7 +1,9 @@
 """GPU parity at the largest per-GPU shares: the Qwen3-32B-shaped share
 (S = 524288, Hq = 8, Hkv = 1, every U) and the 4M-token Llama3-8B share
 (S = 4194304, U = 1).  The oracle checks sampled query rows (O, lse, dQ are
-row-local and exact), the exact dK/dV of the last keys, and the whole-tensor
+row-local and exact), the exact dK/dV of the last keys, dK/dV of interior
+key columns (key 0, tile edges, the middle, seeded random keys) conditioned
+on the GPU's lse and on D = dO.O from the GPU's O, and the whole-tensor
 gradient identities sum_j dK_j = 0 and sum_j dV_j = sum_i dO_i."""
 
 import numpy as np
@@ -28,7 +30,7 @@ def _same_bits(a, b):
     return torch.equal(a.view(torch.int32), b.view(torch.int32))
 
 
-def _check(w, q, k, v, do, o, lse, dq, dk, dv, n_rows, tail):
+def _check(w, q, k, v, do, o, lse, dq, dk, dv, n_rows, tail, n_cols):
     """Only the sampled and tail rows of q and dO are converted to float64."""
     S = w.S
     k64, v64 = as64(k), as64(v)
@@ -43,6 +45,12 @@ def _check(w, q, k, v, do, o, lse, dq, dk, dv, n_rows, tail):
     dk_t, dv_t = A.attn_key_tail_at(as64(q[j0:]), as64(do[j0:]), k64, v64, j0)
     assert_close("dk tail", dk[j0:], dk_t)
     assert_close("dv tail", dv[j0:], dv_t)
+    cols = W.sample_key_cols(S, n_cols, w.seed)
+    print(f"  oracle: {len(cols)} key columns conditioned on the GPU's lse and O", flush=True)
+    dk_c, dv_c = A.attn_key_cols_given(q.float().numpy(), do.float().numpy(), k64, v64,
+                                       o.float().numpy(), lse.numpy(), cols)
+    assert_close("dk cols (conditioned on GPU lse, D)", dk[cols], dk_c)
+    assert_close("dv cols (conditioned on GPU lse)", dv[cols], dv_c)
     # Whole-tensor identities, accumulated in float64 over the bf16 outputs.
     # Bound = unbiased rounding part 0.05 sqrt(S) rms + systematic part
     # 2^-12 sum_j |.|: the fp32 accumulation of v_mfma_f32_32x32x16_bf16 is not
@@ -87,7 +95,7 @@ def test_qwen32b_share_all_chunk_sizes():
             del o, lse, dq, dk, dv
     kept = [t.cpu() for t in ref]
     del ref
-    _check(w, q, k, v, do, *kept, n_rows=128, tail=256)
+    _check(w, q, k, v, do, *kept, n_rows=128, tail=256, n_cols=64)
 
 
 @pytest.mark.timeout(1200)
@@ -105,4 +113,4 @@ def test_llama8b_4m_share():
     torch.cuda.synchronize()
     outs = [t.cpu() for t in (o, lse, dq, dk, dv)]
     del o, lse, dq, dk, dv, qd, kd, vd, dod
-    _check(w, q, k, v, do, *outs, n_rows=32, tail=64)
+    _check(w, q, k, v, do, *outs, n_rows=32, tail=64, n_cols=64)

@@ -164,6 +164,18 @@ def sample_rows(S, n_random, seed):
     return sorted(fixed | set(rnd))
 
 
+def sample_key_cols(S, n, seed):
+    """Key columns for sampled key-gradient checks: the keys with the longest
+    accumulation chains and the tile edges (0, 1, 127, 128), the middle and
+    the last key, filled up to n with seeded random keys."""
+    fixed = {0, 1, 127, 128, S // 2, S - 1}
+    cols = {c for c in fixed if 0 <= c < S}
+    gen = torch.Generator(device="cpu").manual_seed(seed + 2000)
+    while len(cols) < min(n, S):
+        cols.add(int(torch.randint(0, S, (1,), generator=gen)))
+    return sorted(cols)
+
+
 def causal_pairs(S):
     """Number of visible (query, key) pairs of one causal head."""
     return S * (S + 1) // 2
