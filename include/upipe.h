@@ -140,6 +140,26 @@ int upipe_attn_fwd_batch(const void* q, const void* k, const void* v, void* o,
                          hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * upipe_attn_fwd for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ * Same arguments, layouts, results and errors as upipe_attn_fwd, without
+ * the workspace: the library uses a scratch array of its own, a static
+ * device array of upipe_attn_fwd_noalloc_scratch_bytes() bytes (64 MiB) that
+ * each GPU the library runs on holds until the process ends.  Shapes whose
+ * upipe_attn_fwd_workspace_size exceeds it return UPIPE_ERR_WORKSPACE (with
+ * one key/value head and U = 1 that is S up to about 64K tokens).  The call
+ * allocates nothing; its first call on a device looks up that device's
+ * copy of the array (the stream must belong to the current device).  Every
+ * call on one GPU shares that GPU's array: calls that overlap on one GPU
+ * (concurrent streams or host threads) race and must be serialised by the
+ * caller.  Nothing in the array needs clearing between calls.
+ * ---------------------------------------------------------------------- */
+size_t upipe_attn_fwd_noalloc_scratch_bytes(void);
+int upipe_attn_fwd_noalloc(const void* q, const void* k, const void* v, void* o,
+                           float* lse, int64_t S, int Hq, int Hkv, int d, int causal,
+                           int U, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * One ring step of context-parallel attention (Section 2.2, Ring Attention
  * with online softmax; Section 4, the Ulysses + Ring hybrid of USP that
  * UPipe extends): attention of a query block against one key/value block

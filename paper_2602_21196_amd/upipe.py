@@ -50,6 +50,9 @@ _SIGNATURES = {
                                     _c_void_p, _c_void_p, _c_void_p, _c_void_p,
                                     _i64, _i64, _int, _int, _int, _int, _int,
                                     _c_void_p, _size, _c_void_p]),
+    "upipe_attn_fwd_noalloc_scratch_bytes": (_size, []),
+    "upipe_attn_fwd_noalloc": (_int, [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _fptr,
+                                      _i64, _int, _int, _int, _int, _int, _c_void_p]),
     "upipe_attn_fwd_ring_workspace_size": (_size, [_i64, _i64, _int, _int, _int, _int]),
     "upipe_attn_fwd_ring": (_int, [_c_void_p, _c_void_p, _c_void_p, _c_void_p, _fptr,
                                    _i64, _i64, _i64, _i64, _int, _int, _int, _int,
@@ -164,6 +167,14 @@ def upipe_attn_bwd_batch(q, k, v, o, lse, dout, dq, dk, dv, B, S, Hq, Hkv, d,
                          causal, U, ws, ws_bytes, stream):
     return lib().upipe_attn_bwd_batch(q, k, v, o, lse, dout, dq, dk, dv, B, S, Hq,
                                       Hkv, d, causal, U, ws, ws_bytes, stream)
+
+
+def upipe_attn_fwd_noalloc_scratch_bytes():
+    return lib().upipe_attn_fwd_noalloc_scratch_bytes()
+
+
+def upipe_attn_fwd_noalloc(q, k, v, o, lse, S, Hq, Hkv, d, causal, U, stream):
+    return lib().upipe_attn_fwd_noalloc(q, k, v, o, lse, S, Hq, Hkv, d, causal, U, stream)
 
 
 def upipe_attn_fwd_ring_workspace_size(Sq, Skv, Hq, Hkv, d, U):
