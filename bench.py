@@ -54,6 +54,12 @@ def parse():
                    help="layer workloads: rotary base (0 = none); default: the workload's")
     p.add_argument("--cpu-seconds", type=float, default=15.0,
                    help="target CPU time of the oracle sample")
+    p.add_argument("--ceiling", action="store_true",
+                   help="instead of the workload: the sustained bf16 MFMA rate of a large "
+                        "plain GEMM (the library's projection GEMM and torch.matmul), "
+                        "each run back to back for --ceiling-seconds")
+    p.add_argument("--ceiling-size", type=int, default=8192)
+    p.add_argument("--ceiling-seconds", type=float, default=3.0)
     return p.parse_args()
 
 
@@ -190,12 +196,69 @@ def linear_fit(xs, ys):
     return A, B, (1.0 - ss_res / ss_tot) if ss_tot else 1.0
 
 
+def ceiling_bench(args):
+    """Sustained bf16 dense MFMA rate on an MFMA-bound plain GEMM (M = N = K =
+    --ceiling-size, N(0,1) operands, so the matrix units see realistic bit
+    patterns): the library's projection GEMM and torch.matmul (hipBLASLt),
+    each launched back to back for --ceiling-seconds of wall time after a
+    warm-up, so that the chip reaches its sustained (power-limited) clock."""
+    import torch
+    from paper_2602_21196_amd import upipe
+    n = args.ceiling_size
+    g = torch.Generator().manual_seed(77)
+    a = torch.randn((n, n), generator=g).to(torch.bfloat16).to("cuda:0")
+    b = torch.randn((n, n), generator=g).to(torch.bfloat16).to("cuda:0")
+    c = torch.empty((n, n), dtype=torch.bfloat16, device="cuda:0")
+    flops = 2.0 * n * n * n
+    st = torch.cuda.current_stream().cuda_stream
+    pa, pb, pc = a.data_ptr(), b.data_ptr(), c.data_ptr()
+
+    def ours():
+        if upipe.upipe_gemm_bf16(pa, pb, pc, n, n, n, st) != 0:
+            raise RuntimeError("upipe_gemm_bf16 failed")
+
+    def blas():
+        torch.matmul(a, b, out=c)
+
+    res = {}
+    for name, fn in (("upipe_gemm_bf16", ours), ("torch.matmul (hipBLASLt)", blas)):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        # launches per second from a short probe, then one timed run of the
+        # requested length (no host sync inside)
+        t0 = time.perf_counter()
+        for _ in range(10):
+            fn()
+        torch.cuda.synchronize()
+        per = (time.perf_counter() - t0) / 10
+        reps = max(10, int(args.ceiling_seconds / per))
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            fn()
+        torch.cuda.synchronize()
+        el = time.perf_counter() - t0
+        res[name] = {"tflops": round(flops * reps / el / 1e12, 1), "launches": reps,
+                     "seconds": round(el, 2), "ms_per_launch": round(el / reps * 1e3, 3),
+                     "frac_of_peak": round(flops * reps / el / 1e12 / PEAK_BF16_TFLOPS, 4)}
+    best = max(v["tflops"] for v in res.values())
+    out = {"metric": "sustained bf16 dense GEMM TFLOP/s per MI355X (attainable MFMA ceiling)",
+           "value": best, "unit": "TFLOP/s", "n_gpus": 1, "higher_is_better": True,
+           "dtype": "bf16", "data": "synthetic N(0,1)",
+           "config": {"workload": f"gemm M=N=K={n}", "seconds_per_kernel": args.ceiling_seconds},
+           "peak": PEAK_BF16_TFLOPS, "frac_of_peak": round(best / PEAK_BF16_TFLOPS, 4),
+           "kernels": res}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: this build has no multi-GPU "
               f"path (asked for --gpus {args.gpus}).", file=sys.stderr)
         sys.exit(2)
+    if args.ceiling:
+        return ceiling_bench(args)
     import torch
     import workloads as W
     from paper_2602_21196_amd import upipe
@@ -306,6 +369,11 @@ def main():
             "bwd_workspace": round(upipe.upipe_layer_bwd_workspace_size(S, w.d_model, Hq, Hkv,
                                                                          d, U) / 1e9, 4)}
 
+    if not args.no_sweep and w.is_layer and B == 1:
+        del ws_f, ws_b
+        torch.cuda.synchronize()
+        out.update(layer_sweep(args, w, x, wqkv, wo, dy, rope_base, step_flops))
+
     if not args.no_sweep and not w.is_layer and B == 1:
         del ws_f, ws_b
         torch.cuda.synchronize()
@@ -348,6 +416,60 @@ def main():
     if not args.no_cpu_baseline and not w.is_layer and B == 1:
         out["cpu_baseline"] = cpu_baseline(w, q, k, v, do, args.cpu_seconds)
     print(json.dumps(out), flush=True)
+
+
+def layer_sweep(args, w, x, wqkv, wo, dy, rope_base, step_flops):
+    """Throughput and peak activation memory of the layer share for every U.
+
+    Peak = torch.cuda.max_memory_allocated over one forward + backward above
+    the resident inputs (x, weights, dY), minus the caller-owned outputs (y,
+    final_out, lse, dX, dWqkv, dWo): the two workspaces and the kept
+    attention output's lifetime overlap, as a training step would see them.
+    Only the U-dependent chunk buffers change with U (per chunk head the
+    projected Q, the recomputed output and the fp32 lse, D rows), and the
+    dK/dV fp32 carries while a key/value group spans chunks."""
+    import torch
+    from paper_2602_21196_amd import upipe
+    S, Hq, Hkv, d, dm = w.S, w.Hq, w.Hkv, w.d, w.d_model
+    full_ac = args.checkpointing == "full"
+    out_bytes = 2 * S * dm + 2 * S * Hq * d + 4 * Hq * S + 2 * S * dm + \
+        2 * dm * (Hq + 2 * Hkv) * d + 2 * Hq * d * dm
+    mem, tf, ws = {}, {}, {}
+    for u in w.U_sweep:
+        torch.cuda.empty_cache()
+        torch.cuda.synchronize()
+        torch.cuda.reset_peak_memory_stats()
+        base = torch.cuda.memory_allocated()
+        y, o, lse = upipe.layer_fwd(x, wqkv, wo, Hq, Hkv, d, U=u, rope_base=rope_base)
+        g = upipe.layer_bwd(x, wqkv, wo, None if full_ac else o, None if full_ac else lse, dy,
+                            Hq, Hkv, d, U=u, rope_base=rope_base)
+        torch.cuda.synchronize()
+        mem[str(u)] = round((torch.cuda.max_memory_allocated() - base - out_bytes) / 1e9, 4)
+        ws[str(u)] = {"fwd": round(upipe.upipe_layer_fwd_workspace_size(S, dm, Hq, Hkv, d, u)
+                                   / 1e9, 4),
+                      "bwd": round(upipe.upipe_layer_bwd_workspace_size(S, dm, Hq, Hkv, d, u)
+                                   / 1e9, 4)}
+        del y, o, lse, g
+        wf = upipe.workspace(upipe.upipe_layer_fwd_workspace_size(S, dm, Hq, Hkv, d, u), "cuda:0")
+        wb = upipe.workspace(upipe.upipe_layer_bwd_workspace_size(S, dm, Hq, Hkv, d, u), "cuda:0")
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        for _ in range(2):
+            y, o, lse = upipe.layer_fwd(x, wqkv, wo, Hq, Hkv, d, U=u, ws=wf, rope_base=rope_base)
+            g = upipe.layer_bwd(x, wqkv, wo, None if full_ac else o, None if full_ac else lse,
+                                dy, Hq, Hkv, d, U=u, ws=wb, rope_base=rope_base)
+        torch.cuda.synchronize()
+        tf[str(u)] = round(step_flops / ((time.perf_counter() - t1) / 2) / 1e12, 2)
+        del y, o, lse, g, wf, wb
+    us = [int(u) for u in mem]
+    fit_a, fit_b, r2 = linear_fit(us, [mem[str(u)] for u in us])
+    return {"peak_activation_gb_vs_U": mem, "workspace_gb_vs_U": ws,
+            "peak_activation_fit": {"A_gb": round(fit_a, 4), "B_gb_per_U": round(fit_b, 4),
+                                    "r2": round(r2, 4)},
+            "peak_activation_note": (
+                "max_memory_allocated during one layer fwd+bwd above the resident "
+                "inputs, minus the outputs y, final_out, lse, dX, dWqkv, dWo"),
+            "tflops_vs_U": tf}
 
 
 def ring_cpu_baseline(w, q, k, v, delta, target_s):

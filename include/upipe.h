@@ -323,6 +323,17 @@ int upipe_layer_bwd_ex(const void* x, const void* wqkv, const void* wo,
                        size_t ws_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * The block's projection product on its own (Appendix A: the QKV projection
+ * and y = final_out wo are products of this form): c = a b with a bf16
+ * [M, K] and b bf16 [K, N] row-major, c bf16 [M, N] row-major, fp32
+ * accumulation in ascending k, one rounding.  M, N, K multiples of 128 and at
+ * most 65536 (UPIPE_ERR_UNSUPPORTED otherwise).  For callers that project
+ * outside the block, and to measure the GEMM kernel alone.  No workspace.
+ * ---------------------------------------------------------------------- */
+int upipe_gemm_bf16(const void* a, const void* b, void* c, int64_t M, int64_t N,
+                    int64_t K, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * Kernel timing (measurement aid).  While enabled, every kernel the library
  * launches is bracketed by two HIP events recorded on the launch stream.
  * upipe_profile_query() waits for the recorded events and reports, for the

@@ -8,11 +8,9 @@
 //   K-major operand  (k contiguous)    : rows = m (or n), 128 k per row;
 //   MN-major operand (m/n contiguous)  : rows = k, 128 m (or n) per row --
 // by buffer->LDS copies (no register staging), and the MFMA fragments are
-// read in one common k order:
-//   two K-major operands       : plain 16-byte reads (k = 8g + 0..7);
-//   an MN-major operand        : transposing reads (tr_operand, k = 4g + 0..3,
-//                                8 + 4g + 0..3), and a K-major partner then
-//                                reads the same k as two 8-byte halves.
+// read in one common k order, k = 8g + 0..7 within each 16-k step:
+//   a K-major operand          : plain 16-byte reads;
+//   an MN-major operand        : transposing reads (tr_operand_k8).
 // Operands may be split into 128-wide blocks with their own stride (the
 // head-major chunk buffers [U][Sp][128]).
 //
@@ -66,19 +64,26 @@ __device__ __forceinline__ void lane_offsets(int64_t ld, int w, int lane, uint32
   }
 }
 
-// Fragment of the 32 rows (m or n) r0.. at k-step ks (16 k) of one tile.
-//   KM_PLAIN: K-major tile, k = 16 ks + 8g + 0..7
-//   KM_TR   : K-major tile, k = 16 ks + 4g + 0..3, 16 ks + 8 + 4g + 0..3
-//   MN      : MN-major tile (transposing reads), same k order as KM_TR
-enum { KM_PLAIN = 0, KM_TR = 1, MN_TR = 2 };
-template <int MODE>
-__device__ __forceinline__ bf16x8 frag(const char* tile, int r0, int ks, int lane) {
-  const int r32 = lane & 31, g = lane >> 5;
-  if (MODE == KM_PLAIN) return lds_read_b128(tile, swzt(r0 + r32, 2 * ks + g));
-  if (MODE == MN_TR) return tr_operand(tile, 16 * ks, r0, lane);
+// MN-major operand fragment: the 32 columns r0.. of a [k][128] tile at
+// k-step ks, lane l getting column r0 + (l % 32) at k = 16 ks + 8g + 0..7
+// (g = l / 32) -- eight consecutive k, so that a K-major partner reads the
+// same k as one plain 16-byte chunk.  (The attention kernels' tr_operand
+// takes k = 4g + 0..3, 8 + 4g + 0..3 instead, the row order of an MFMA
+// result tile; here both operands come from LDS and only have to agree.)
+// Two ds_read_b64_tr_b16 per lane: within each 16-lane group, loader lane t
+// reads the 8 bytes at row 16 ks + 8g + t/4 (+ 4 for the second read),
+// columns r0 + 16 ((l >> 4) & 1) + 4 (t % 4); with the swzt swizzle the
+// 8 rows x 4 chunks of one read fill every bank exactly twice.
+__device__ __forceinline__ bf16x8 tr_operand_k8(const char* tile, int ks, int r0, int lane) {
   typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
-  const bf16x4 lo = *(const lds_bf16x4*)(tile + swzt(r0 + r32, 2 * ks) + 8 * g);
-  const bf16x4 up = *(const lds_bf16x4*)(tile + swzt(r0 + r32, 2 * ks + 1) + 8 * g);
+  const int t = lane & 15, hi = (lane >> 4) & 1, g = lane >> 5;
+  const int col = r0 + 16 * hi + 4 * (t & 3);
+  const int row = 16 * ks + 8 * g + (t >> 2);
+  const uint32_t cb = (uint32_t)(col & 7) << 1;   // byte offset inside the 16-byte chunk
+  const bf16x4 lo =
+      __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(tile + swzt(row, col >> 3) + cb));
+  const bf16x4 up =
+      __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(tile + swzt(row + 4, col >> 3) + cb));
   bf16x8 v;
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
@@ -86,6 +91,19 @@ __device__ __forceinline__ bf16x8 frag(const char* tile, int r0, int ks, int lan
     v[4 + e] = up[e];
   }
   return v;
+}
+
+// Fragment of the 32 rows (m or n) r0.. at k-step ks (16 k) of one tile, in
+// the k order k = 16 ks + 8g + 0..7 shared by both modes:
+//   KM: K-major tile, one plain 16-byte read (chunk 2 ks + g of the row)
+//   MN: MN-major tile, transposing reads (tr_operand_k8)
+// The plain reads of 32 rows x 2 chunks touch each bank once per 16 lanes.
+enum { KM = 0, MN = 1 };
+template <int MODE>
+__device__ __forceinline__ bf16x8 frag(const char* tile, int r0, int ks, int lane) {
+  const int r32 = lane & 31, g = lane >> 5;
+  if (MODE == KM) return lds_read_b128(tile, swzt(r0 + r32, 2 * ks + g));
+  return tr_operand_k8(tile, ks, r0, lane);
 }
 
 // One stage of LDS (64 KB) per workgroup, so that two workgroups share a CU:
@@ -102,8 +120,8 @@ template <bool A_K, bool B_K, int EPI>
 __global__ __launch_bounds__(256, 3 - GemmStages<EPI>::N) void gemm_kernel(
     GemmOperand A, GemmOperand B, GemmEpilogue E, int64_t M, int64_t N, int64_t k_begin,
     int64_t k_len) {
-  constexpr int AM = A_K ? (B_K ? KM_PLAIN : KM_TR) : MN_TR;
-  constexpr int BMODE = B_K ? (A_K ? KM_PLAIN : KM_TR) : MN_TR;
+  constexpr int AM = A_K ? KM : MN;
+  constexpr int BMODE = B_K ? KM : MN;
   constexpr int NST = GemmStages<EPI>::N;
   __shared__ __attribute__((aligned(1024))) char smem[NST * 2 * TILE_BYTES];
   const int t = threadIdx.x;

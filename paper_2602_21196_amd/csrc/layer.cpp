@@ -407,6 +407,23 @@ int upipe_layer_bwd_ex(const void* x, const void* wqkv, const void* wo, const vo
   }
 }
 
+int upipe_gemm_bf16(const void* a, const void* b, void* c, int64_t M, int64_t N, int64_t K,
+                    hipStream_t stream) {
+  try {
+    if (M < 1 || N < 1 || K < 1) return UPIPE_ERR_INVALID_ARG;
+    if (M % 128 || N % 128 || K % 128) return UPIPE_ERR_UNSUPPORTED;
+    if (M > 65536 || N > 65536 || K > 65536) return UPIPE_ERR_UNSUPPORTED;
+    if (!aligned16(a) || !aligned16(b) || !aligned16(c)) return UPIPE_ERR_INVALID_ARG;
+    // A [M, K] row-major is K-major; B [K, N] row-major is N-major.
+    UPIPE_LAUNCH(kGemm, stream,
+                 gemm1(operand((const bf16*)a, K, M, K), true, operand((const bf16*)b, N, N, K),
+                       false, store_epi((bf16*)c, N, M), GEMM_EPI_ACC32, M, N, K, stream));
+    return UPIPE_OK;
+  } catch (...) {
+    return UPIPE_ERR_HIP;
+  }
+}
+
 int upipe_layer_fwd(const void* x, const void* wqkv, const void* wo, void* y, void* o_saved,
                     float* lse_saved, int64_t S, int d_model, int Hq, int Hkv, int d, int U,
                     void* ws, size_t ws_bytes, hipStream_t stream) {

@@ -74,6 +74,8 @@ _SIGNATURES = {
                                   _c_void_p, _c_void_p, _c_void_p, _c_void_p,
                                   _i64, _i64, _int, _int, _int, _int, _int, _dbl, _i64,
                                   _c_void_p, _size, _c_void_p]),
+    "upipe_gemm_bf16": (_int, [_c_void_p, _c_void_p, _c_void_p, _i64, _i64, _i64,
+                               _c_void_p]),
     "upipe_profile_enable": (_int, [_int]),
     "upipe_profile_reset": (_int, []),
     "upipe_profile_query": (_int, [ctypes.c_char_p, ctypes.POINTER(_int),
@@ -222,6 +224,10 @@ def upipe_layer_bwd_ex(x, wqkv, wo, o_saved, lse_saved, dy, dx, dwqkv, dwo, B, S
     return lib().upipe_layer_bwd_ex(x, wqkv, wo, o_saved, lse_saved, dy, dx,
                                     dwqkv, dwo, B, S, d_model, Hq, Hkv, d, U,
                                     rope_base, pos0, ws, ws_bytes, stream)
+
+
+def upipe_gemm_bf16(a, b, c, M, N, K, stream):
+    return lib().upipe_gemm_bf16(a, b, c, M, N, K, stream)
 
 
 def upipe_profile_enable(on):
@@ -513,3 +519,19 @@ def layer_bwd(x, wqkv, wo, o_saved, lse_saved, dy, Hq, Hkv, d=128, U=1,
                                 ws.data_ptr(), ws.numel(), _stream())
         _check("upipe_layer_bwd_ex", st)
     return dx, dwqkv, dwo
+
+
+def gemm(a, b):
+    """c [M,N] = a [M,K] . b [K,N], bf16 with fp32 accumulation (M, N, K
+    multiples of 128)."""
+    torch = _torch()
+    if a.dim() != 2 or b.dim() != 2 or a.shape[1] != b.shape[0]:
+        raise ValueError(f"gemm: a [M,K] and b [K,N], got {tuple(a.shape)}, {tuple(b.shape)}")
+    M, K = a.shape
+    N = b.shape[1]
+    c = torch.empty((M, N), dtype=torch.bfloat16, device=a.device)
+    bf = torch.bfloat16
+    st = upipe_gemm_bf16(_ptr(a, bf, "a"), _ptr(b, bf, "b"), _ptr(c, bf, "c"), M, N, K,
+                         _stream())
+    _check("upipe_gemm_bf16", st)
+    return c

@@ -368,3 +368,18 @@ def test_torch_wrappers_check_every_shape():
         upipe.attn_fwd(q, k, k)
     with pytest.raises(ValueError, match="GPU"):
         upipe.layer_bwd(x, wqkv, wo, _cpu(S, Hq, d), lse, x, Hq, Hkv)
+
+
+def test_gemm_entry_point_validates():
+    INV, UNS = -1, -2
+    g = upipe.upipe_gemm_bf16
+    assert g(FAKE, FAKE, FAKE, 0, 128, 128, None) == INV
+    assert g(FAKE, FAKE, FAKE, 128, 128, -128, None) == INV
+    assert g(FAKE, FAKE, FAKE, 100, 128, 128, None) == UNS
+    assert g(FAKE, FAKE, FAKE, 128, 128, 200, None) == UNS
+    assert g(FAKE, FAKE, FAKE, 128, 65536 + 128, 128, None) == UNS
+    assert g(None, FAKE, FAKE, 128, 128, 128, None) == INV
+    assert g(FAKE, FAKE, FAKE + 2, 128, 128, 128, None) == INV
+    import torch
+    with pytest.raises(ValueError, match="gemm"):
+        upipe.gemm(_cpu(128, 256), _cpu(128, 128))
