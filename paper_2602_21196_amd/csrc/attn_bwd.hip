@@ -1,7 +1,8 @@
 // Causal GQA flash-attention backward for gfx950 (one head chunk per launch).
 //
 // Analytic gradient of softmax attention (paper Section 2.1), with the
-// probabilities rebuilt from the saved row log-sum-exp:
+// probabilities rebuilt from the saved row log-sum-exp (staged as -sqrt(d) lse,
+// the initial value of each row's score accumulator):
 //   P_ij  = exp(q_i.k_j/sqrt d - lse_i),   D_i = dO_i . O_i
 //   dS_ij = P_ij (dO_i . v_j - D_i)
 //   dV_j += sum_i P_ij dO_i,   dK_j += sum_i dS_ij q_i / sqrt d,
@@ -101,22 +102,35 @@ __device__ __forceinline__ void read_dvdk(const char* buf, int sub, int lane, Fr
     }
 }
 
-// S^T and D - dP^T of one subtile from its fragments (16 MFMAs).  The dP
-// accumulators start from the staged D rows (loaded straight into them) and
-// the value fragments come negated, so the chain ends at D - dP and dS needs
-// no subtraction: P (D - dP) = -dS.
-__device__ __forceinline__ void subtile_sdp(const Frags& fr, const bf16x8 (&kf)[8],
-                                            const bf16x8 (&nvf)[8], const char* buf, int sub,
-                                            int g, f32x16& sacc, f32x16& pacc) {
+// Accumulator seeds of the 32-row subtile at rows `sub`.. of the tile, in the
+// MFMA C layout (element 4a + b is row sub + 8a + 4g + b), loaded from the
+// staged rows straight into the accumulators: the score accumulator starts at
+// -sqrt(d) lse of its row, so that it ends at q.k - sqrt(d) lse and
+// P = exp2(acc log2(e) / sqrt(d)) needs no lse term; the dP accumulator
+// starts at D, and the value fragments come negated, so that chain ends at
+// D - dP and dS needs no subtraction: P (D - dP) = -dS.  A pair's seeds are
+// read before its fragments: LDS reads complete in order, and a seed read
+// behind a burst of fragment reads would wait for the whole burst.
+__device__ __forceinline__ void subtile_seed(const char* buf, int sub, int g, f32x16& sacc,
+                                             f32x16& pacc) {
   const float* Dl = reinterpret_cast<const float*>(buf + OFF_D) + sub;
+  const float* Ll = reinterpret_cast<const float*>(buf + OFF_LSE) + sub;
 #pragma unroll
   for (int a = 0; a < 4; ++a) {
     const f32x4 d4 = *reinterpret_cast<const f32x4*>(Dl + 8 * a + 4 * g);
+    const f32x4 l4 = *reinterpret_cast<const f32x4*>(Ll + 8 * a + 4 * g);
 #pragma unroll
-    for (int b = 0; b < 4; ++b) pacc[4 * a + b] = d4[b];
+    for (int b = 0; b < 4; ++b) {
+      pacc[4 * a + b] = d4[b];
+      sacc[4 * a + b] = l4[b];
+    }
   }
-#pragma unroll
-  for (int i = 0; i < 16; ++i) sacc[i] = 0.f;
+}
+
+// S^T and D - dP^T of one subtile from its fragments (16 MFMAs), on top of
+// the seeds.
+__device__ __forceinline__ void subtile_sdp(const Frags& fr, const bf16x8 (&kf)[8],
+                                            const bf16x8 (&nvf)[8], f32x16& sacc, f32x16& pacc) {
 #pragma unroll
   for (int s = 0; s < 8; ++s) {
     sacc = mfma32x32x16(fr.f[2 * s], kf[s], sacc);
@@ -124,20 +138,15 @@ __device__ __forceinline__ void subtile_sdp(const Frags& fr, const bf16x8 (&kf)[
   }
 }
 
-// P and -dS of one subtile (rows `sub`.. of the tile) as bf16 A operands,
-// from its scores, the staged lse rows and D - dP.  Negation is exact and
-// commutes with rounding, so the dK accumulators carry exactly -dK (the
-// final scale is -1/sqrt d).  No masking here (subtile_mask).
-__device__ __forceinline__ void subtile_pds(const f32x16& sacc, const f32x16& pacc, const char* buf,
-                                            int sub, int g, bf16x8 (&pf)[2], bf16x8 (&sf)[2]) {
-  const float* lsel = reinterpret_cast<const float*>(buf + OFF_LSE) + sub;
+// P and -dS of one subtile as bf16 A operands, from its lse-seeded scores
+// and D - dP.  Negation is exact and commutes with rounding, so the dK
+// accumulators carry exactly -dK (the final scale is -1/sqrt d).  No masking
+// here (subtile_mask).
+__device__ __forceinline__ void subtile_pds(const f32x16& sacc, const f32x16& pacc,
+                                            bf16x8 (&pf)[2], bf16x8 (&sf)[2]) {
   float p[16];
 #pragma unroll
-  for (int a = 0; a < 4; ++a) {
-    const f32x4 l4 = *reinterpret_cast<const f32x4*>(lsel + 8 * a + 4 * g);
-#pragma unroll
-    for (int b = 0; b < 4; ++b) p[4 * a + b] = fast_exp2(fmaf(sacc[4 * a + b], kSl2, -l4[b]));
-  }
+  for (int i = 0; i < 16; ++i) p[i] = fast_exp2(sacc[i] * kSl2);
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
     pf[i >> 3][i & 7] = (bf16)p[i];
@@ -221,20 +230,23 @@ __device__ __forceinline__ void pair_step(const char* buf, int base, uint32_t qb
   f32x16 s1, p1, s0, p0;
   bf16x8 pf1[2], sf1[2], pf0[2], sf0[2];
   const uint32_t q1 = qb + base + 32, q0 = qb + base;
+  subtile_seed(buf, base + 32, g, s1, p1);
+  subtile_seed(buf, base, g, s0, p0);
+  __builtin_amdgcn_sched_barrier(0);
   read_sdp(buf, base, r32, g, fb);
   __builtin_amdgcn_sched_barrier(0);
-  subtile_sdp(fa, kf, vf, buf, base + 32, g, s1, p1);                                            // A
+  subtile_sdp(fa, kf, vf, s1, p1);                                            // A
   read_dvdk(buf, base + 32, lane, fa);
   interleave_mfma_lds<2>();
   __builtin_amdgcn_sched_barrier(0);
-  subtile_sdp(fb, kf, vf, buf, base, g, s0, p0);                                            // B
-  subtile_pds(s1, p1, buf, base + 32, g, pf1, sf1);
+  subtile_sdp(fb, kf, vf, s0, p0);                                            // B
+  subtile_pds(s1, p1, pf1, sf1);
   interleave_mfma_valu();
   __builtin_amdgcn_sched_barrier(0);
   subtile_mask<CAUSAL>(q1, mykey, q1 < kw + 31, g, pf1, sf1);
   dvdk_products(fa, pf1, sf1, dva, dka);                                      // C
   read_dvdk(buf, base, lane, fb);
-  subtile_pds(s0, p0, buf, base, g, pf0, sf0);
+  subtile_pds(s0, p0, pf0, sf0);
   interleave_mfma_valu();
   __builtin_amdgcn_sched_barrier(0);
   subtile_mask<CAUSAL>(q0, mykey, q0 < kw + 31, g, pf0, sf0);
@@ -451,7 +463,7 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_kernel(
   issue_kstage(rk, rv, offk, offv, 0, smem, w);
 
   bf16x8 qf[8], df[8];
-  float lse2 = 0.f, Dq = 0.f;
+  float nlse = 0.f, Dq = 0.f;
 #pragma unroll
   for (int s = 0; s < 8; ++s)
 #pragma unroll
@@ -463,7 +475,7 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_kernel(
       qf[s] = *reinterpret_cast<const bf16x8*>(Qc + rowoff + 16 * s);
       df[s] = *reinterpret_cast<const bf16x8*>(dOc + rowoff + 16 * s);
     }
-    lse2 = lse_c[(int64_t)u * Sp + myq];   // already times log2(e)
+    nlse = lse_c[(int64_t)u * Sp + myq];   // -sqrt(d) lse: the score accumulator's seed
     Dq = Dc[(int64_t)u * Sp + myq];
   }
 
@@ -488,7 +500,7 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_kernel(
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) { sacc[hh][i] = 0.f; pacc[hh][i] = 0.f; }
+        for (int i = 0; i < 16; ++i) { sacc[hh][i] = nlse; pacc[hh][i] = 0.f; }
 #pragma unroll
       for (int s = 0; s < 8; ++s)
 #pragma unroll
@@ -503,7 +515,7 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_kernel(
       for (int hh = 0; hh < 2; ++hh) {
         float p[16];
 #pragma unroll
-        for (int i = 0; i < 16; ++i) p[i] = fast_exp2(fmaf(sacc[hh][i], kSl2, -lse2));
+        for (int i = 0; i < 16; ++i) p[i] = fast_exp2(sacc[hh][i] * kSl2);
         if (diag) {   // wave-uniform
 #pragma unroll
           for (int i = 0; i < 16; ++i) {

@@ -16,7 +16,7 @@ hipError_t launch_pack_rows(const bf16* src, int64_t S, int H, int h0, int n,
 // src [n, Sp, d] rows < S  ->  dst [S, H, d] heads h0..h0+n-1.
 hipError_t launch_unpack_rows(const bf16* src, int64_t S, int H, int h0, int n,
                               int64_t Sp, bf16* dst, hipStream_t st);
-// D[n, Sp] = rowsum(a * b) over the head width and lse_c[n, Sp] = log2(e)
+// D[n, Sp] = rowsum(a * b) over the head width and lse_c[n, Sp] = -sqrt(d)
 // times the lse rows h0.. of the caller's [Hq, S] array (zero for rows >= S).  Element
 // (s, hh, e) of a is a[s * a_row + hh * a_head + e], likewise for b.
 hipError_t launch_rowdot_lse(const bf16* a, int64_t a_row, int64_t a_head,
@@ -51,7 +51,8 @@ hipError_t launch_lse_merge(bf16* o, float* lse, const bf16* o_p,
                             hipStream_t st);
 
 // ---- attention backward (attn_bwd.hip) -----------------------------------
-// lse_c below holds log2(e) * lse (the kernels evaluate exp2).
+// lse_c below holds -sqrt(d) lse, the initial value of a row's score
+// accumulator (the kernels evaluate P = exp2(acc log2(e) / sqrt(d))).
 // Key/value gradients of the chunk's heads, accumulated in fp32 on top of
 // dK32/dV32 [Hkv, Sp, d] (read unless the chunk holds a group's first head;
 // dK32 carries the unscaled sum with its sign flipped, -sum dS^T Q), written

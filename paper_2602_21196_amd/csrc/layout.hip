@@ -51,8 +51,10 @@ __global__ __launch_bounds__(256) void unpack_rows_kernel(
 }
 
 // D[hh][s] = sum_e dO(s, hh, e) * O(s, hh, e) in fp32 (the backward's row
-// term) and the chunk's log-sum-exp rows, multiplied by log2(e) for the
-// kernels' exp2, copied to a padded buffer.  Element
+// term) and the chunk's log-sum-exp rows times -sqrt(d) (the initial value
+// of the backward kernels' score accumulators: they end at
+// q.k - sqrt(d) lse, so P = exp2(acc log2(e) / sqrt(d))), copied to a padded
+// buffer.  Element
 // (s, hh, e) of an operand X lives at X + s * x_row + hh * x_head + e.  One
 // wave per (row, head); lanes hold two elements each and reduce by shuffles.
 __global__ __launch_bounds__(256) void rowdot_lse_kernel(
@@ -70,7 +72,7 @@ __global__ __launch_bounds__(256) void rowdot_lse_kernel(
     const bf16* pa = a + s * a_row + hh * a_head + 2 * lane;
     const bf16* pb = b + s * b_row + hh * b_head + 2 * lane;
     acc = (float)pa[0] * (float)pb[0] + (float)pa[1] * (float)pb[1];
-    l = lse[(int64_t)(h0 + hh) * S + s] * 1.4426950408889634f;
+    l = lse[(int64_t)(h0 + hh) * S + s] * -11.313708498984761f;   // -sqrt(128) lse
   }
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) acc += __shfl_xor(acc, off);
