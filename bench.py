@@ -105,6 +105,23 @@ def measured_traffic(kernel, workload, U):
     return rec["fetch_bytes"] + rec["write_bytes"]
 
 
+def measured_clock(kernel, workload, U):
+    """Sustained shader clock (GHz) under a kernel from profiles/clock.json
+    (rocprofv3 GRBM_COUNT per dispatch over its kernel-trace duration, per
+    XCD), if it was taken on the current source of that kernel for this
+    workload; else None."""
+    import json as _json
+    path = os.path.join(ROOT, "profiles", "clock.json")
+    try:
+        with open(path) as f:
+            rec = _json.load(f).get(f"{workload}/U{U}/{kernel}")
+    except (OSError, ValueError):
+        return None
+    if not rec or rec.get("source_sha") != source_sha(kernel):
+        return None
+    return rec["clock_ghz"]
+
+
 def host_info():
     """(BLAS threads in use, BLAS library, CPU model) of this host."""
     cores, blas = os.cpu_count(), "unknown"
@@ -347,7 +364,12 @@ def main():
                 "frac": round(achieved / PEAK_BF16_TFLOPS, 4) if achieved else None,
                 "traffic": (measured_traffic(dom, w.name, U)
                             if dom in KERNEL_SOURCES else None),
-                "traffic_unit": "bytes per launch"}
+                "traffic_unit": "bytes per launch",
+                "clock_ghz_est": (measured_clock(dom, w.name, U)
+                                  if dom in KERNEL_SOURCES else None),
+                "clock_note": "sustained shader clock under this kernel (rocprofv3 "
+                              "GRBM_COUNT / duration / 8 XCDs, profiles/clock.json); "
+                              "the peak assumes 2.4 GHz"}
     upipe.upipe_profile_reset()
 
     out = {"metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s",
