@@ -151,3 +151,32 @@ def dwo_given_output(o, dy, cols):
     S = o.shape[0]
     dyc = np.asarray(dy[:, cols], np.float64)
     return o.reshape(S, -1).T @ dyc
+
+
+def attention_inputs(x, wqkv, wo, dy, Hq, Hkv, d, rope_base=None, pos0=0):
+    """The attention operands of the block's backward (the first steps of
+    ``layer_bwd``): q, k (rotated when ``rope_base`` is given), v and the
+    gradient of final_out dO = dY wo^T, each [S, H, d] in float64."""
+    x = np.asarray(x, np.float64)
+    S = x.shape[0]
+    q, k, v = split_qkv(x @ np.asarray(wqkv, np.float64), Hq, Hkv, d)
+    q = _rotate(q, S, rope_base, pos0)
+    k = _rotate(k, S, rope_base, pos0)
+    do = (np.asarray(dy, np.float64) @ np.asarray(wo, np.float64).T).reshape(S, Hq, d)
+    return q, k, v, do
+
+
+def dwqkv_given_grads(x, dq, dk, dv, cols, rope_base=None, pos0=0):
+    """Columns ``cols`` of dWqkv = x^T [dQ | dK | dV] for given attention
+    gradients with respect to the (rotated) q, k and to v, each [S, H, d]:
+    the gradients of the rotated q, k are turned back first (the chain rule
+    of the rotation).  With the oracle's own gradients this is the oracle's
+    dWqkv; with another implementation's it is the weight gradient those
+    imply ("conditioned" on them).  Returns [d_model, len(cols)]."""
+    x = np.asarray(x, np.float64)
+    S = x.shape[0]
+    dq = _rotate(np.asarray(dq, np.float64), S, rope_base, pos0, inverse=True)
+    dk = _rotate(np.asarray(dk, np.float64), S, rope_base, pos0, inverse=True)
+    dqkv = np.concatenate([dq.reshape(S, -1), dk.reshape(S, -1),
+                           np.asarray(dv, np.float64).reshape(S, -1)], axis=1)
+    return x.T @ dqkv[:, cols]

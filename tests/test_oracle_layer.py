@@ -92,3 +92,33 @@ def test_dwo_given_output_matches_torch_autograd():
     cols = np.array([0, 5, 23])
     np.testing.assert_allclose(L.dwo_given_output(o, dy, cols), dwo_t[:, cols], rtol=0,
                                atol=1e-10)
+
+
+def test_dwqkv_given_grads_matches_torch_autograd():
+    """The weight gradient of Wqkv from the attention gradients (the chain
+    rule through the projection) equals torch float64 autograd's dWqkv."""
+    S, dm, Hq, Hkv, d = 45, 24, 4, 2, 6
+    x, wqkv, wo, dy = _layer_inputs(14, S, dm, Hq, Hkv, d)
+    _, _, dw_t, _ = _torch_layer(x, wqkv, wo, dy, Hq, Hkv, d)
+    from oracle import attention as A
+    q, k, v, do = L.attention_inputs(x, wqkv, wo, dy, Hq, Hkv, d)
+    dq, dk, dv = A.attn_bwd(q, k, v, do)
+    cols = np.array([0, 3, Hq * d, (Hq + Hkv) * d + 1, (Hq + 2 * Hkv) * d - 1])
+    np.testing.assert_allclose(L.dwqkv_given_grads(x, dq, dk, dv, cols), dw_t[:, cols],
+                               rtol=0, atol=1e-10)
+
+
+def test_dwqkv_given_grads_with_rope_matches_full_backward():
+    S, dm, Hq, Hkv, d = 50, 16, 2, 1, 8
+    x, wqkv, wo, dy = _layer_inputs(15, S, dm, Hq, Hkv, d)
+    _, dw, _ = L.layer_bwd(x, wqkv, wo, dy, Hq, Hkv, d, rope_base=100.0, pos0=3)
+    from oracle import attention as A
+    q, k, v, do = L.attention_inputs(x, wqkv, wo, dy, Hq, Hkv, d, rope_base=100.0, pos0=3)
+    dq, dk, dv = A.attn_bwd(q, k, v, do)
+    cols = np.arange(dw.shape[1])
+    got = L.dwqkv_given_grads(x, dq, dk, dv, cols, rope_base=100.0, pos0=3)
+    np.testing.assert_allclose(got, dw, rtol=0, atol=1e-10)
+    # the gradients of the rotated q, k must be turned back: without the
+    # inverse rotation the Q and K columns are wrong
+    bad = L.dwqkv_given_grads(x, dq, dk, dv, cols)
+    assert np.abs(bad[:, :(Hq + Hkv) * d] - dw[:, :(Hq + Hkv) * d]).max() > 1e-3

@@ -90,7 +90,8 @@ def test_layer_llama_width_short_sequence():
 def test_llama8b_layer_share_sampled():
     """The Llama3-8B layer share (S = 256K, d_model = 4096, RoPE with Llama 3's
     base): bitwise equal across U and between kept and recomputed attention
-    output; sampled rows and the key tail against the oracle."""
+    output; sampled rows, the dX tail, and weight-gradient columns over the
+    whole sequence against the oracle."""
     w = W.WORKLOADS["llama8b_layer"]
     S, dm, Hq, Hkv, d = w.S, w.d_model, w.Hq, w.Hkv, w.d
     base = w.extra.get("rope_base")
@@ -132,6 +133,31 @@ def test_llama8b_layer_share_sampled():
     print(f"oracle dwo: {len(cols)} columns conditioned on the GPU's o_saved", flush=True)
     assert_close("dwo cols (conditioned on GPU o_saved)", dwo[:, cols],
                  L.dwo_given_output(o.float().numpy(), dy64, cols), rms_scaled=True)
+    # dWqkv over the whole sequence (the same split-K path) on sampled columns
+    # of the Q, K and V groups, conditioned on attention gradients: the
+    # attention entry points of this library run on bf16 q, k, v, dO that the
+    # oracle forms in float64 from x, Wqkv, Wo and dY, and the oracle takes
+    # x^T [dQ | dK | dV] of their output (rotated gradients turned back).
+    print("oracle dwqkv: attention operands in float64", flush=True)
+    qa, ka, va, doa = L.attention_inputs(x64, w64, wo64, dy64, Hq, Hkv, d, rope_base=base)
+    up = _upipe()
+    ops = [torch.from_numpy(t).to(torch.bfloat16).to(DEV) for t in (qa, ka, va, doa)]
+    del qa, ka, va, doa
+    o_a, lse_a = up.attn_fwd(ops[0], ops[1], ops[2], U=1)
+    grads = up.attn_bwd(ops[0], ops[1], ops[2], o_a, lse_a, ops[3], U=1)
+    torch.cuda.synchronize()
+    dq_a, dk_a, dv_a = (as64(t) for t in grads)
+    del ops, o_a, lse_a, grads
+    qcols = W.sample_key_cols(Hq * d, 24, w.seed)
+    kcols = [Hq * d + c for c in W.sample_key_cols(Hkv * d, 20, w.seed + 1)]
+    vcols = [(Hq + Hkv) * d + c for c in W.sample_key_cols(Hkv * d, 20, w.seed + 2)]
+    cols = qcols + kcols + vcols
+    print(f"oracle dwqkv: {len(cols)} columns", flush=True)
+    ref = L.dwqkv_given_grads(x64, dq_a, dk_a, dv_a, cols, rope_base=base)
+    nq, nk = len(qcols), len(kcols)
+    assert_close("dwqkv cols (conditioned on attention-entry-point dQ, dK, dV)", dwqkv[:, cols],
+                 ref, rms_scaled=True,
+                 blocks=[slice(0, nq), slice(nq, nq + nk), slice(nq + nk, len(cols))])
 
 
 @pytest.mark.parametrize("S,dm,Hq,Hkv,base", [(300, 256, 4, 1, 0.0), (513, 384, 4, 2, 5e5),
