@@ -149,7 +149,8 @@ int upipe_attn_fwd_batch(const void* q, const void* k, const void* v, void* o,
  * upipe_attn_fwd_workspace_size exceeds it return UPIPE_ERR_WORKSPACE (with
  * one key/value head and U = 1 that is S up to about 64K tokens).  The call
  * allocates nothing; its first call on a device looks up that device's
- * copy of the array (the stream must belong to the current device).  Every
+ * copy of the array.  The stream must belong to the current device
+ * (UPIPE_ERR_INVALID_ARG otherwise).  Every
  * call on one GPU shares that GPU's array: calls that overlap on one GPU
  * (concurrent streams or host threads) race and must be serialised by the
  * caller.  Nothing in the array needs clearing between calls.

@@ -31,10 +31,15 @@ std::mutex g_scratch_mu;
 char* g_scratch_ptr[kMaxDevices] = {};
 
 // Device address of `scratch` on the current device, looked up on the first
-// call there; UPIPE_ERR_HIP if the lookup fails.
-int scratch_on_current_device(char** out) {
+// call there; UPIPE_ERR_HIP if the lookup fails, UPIPE_ERR_INVALID_ARG if
+// `stream` belongs to another device (the kernels would run there with this
+// device's scratch address).
+int scratch_on_current_device(hipStream_t stream, char** out) {
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return UPIPE_ERR_HIP;
+  hipDevice_t sdev = -1;
+  if (hipStreamGetDevice(stream, &sdev) != hipSuccess) return UPIPE_ERR_HIP;
+  if (sdev != dev) return UPIPE_ERR_INVALID_ARG;
   std::lock_guard<std::mutex> lock(g_scratch_mu);
   if (g_scratch_ptr[dev] == nullptr) {
     void* p = nullptr;
@@ -67,7 +72,7 @@ int upipe_attn_fwd_noalloc(const void* q, const void* k, const void* v, void* o,
       return UPIPE_ERR_INVALID_ARG;
     if (plan_attn_fwd(S, Hq, Hkv, U).total > kScratchBytes) return UPIPE_ERR_WORKSPACE;
     char* ws = nullptr;
-    rc = scratch_on_current_device(&ws);
+    rc = scratch_on_current_device(stream, &ws);
     if (rc != UPIPE_OK) return rc;
     return run_attn_fwd((const bf16*)q, (const bf16*)k, (const bf16*)v, (bf16*)o, lse, S, Hq,
                         Hkv, causal, U, ws, stream);
