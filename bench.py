@@ -271,7 +271,7 @@ def ceiling_bench(args):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only: this build has no multi-GPU "
+        print(f"bench.py measures one GPU only: this library has no multi-GPU "
               f"path (asked for --gpus {args.gpus}).", file=sys.stderr)
         sys.exit(2)
     if args.ceiling:

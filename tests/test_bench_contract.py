@@ -1,6 +1,6 @@
 """bench.py keeps its output contract: one JSON line with the metric, the
 roofline of the dominant kernel and the oracle's CPU baseline; more than one
-GPU is refused with a message (this build measures one GPU)."""
+GPU is refused with a message (the library measures one GPU)."""
 
 import json
 import os
