@@ -205,6 +205,21 @@ def pin_gqa_equals_repeated_mha(A):
                                atol=1e-12)
 
 
+def pin_key_cols_given_statistics(A):
+    """The conditioned key-column gradient, given the module's own row
+    statistics, against torch float64 autograd (GQA, causal, with key 0 and
+    the diagonal key of the last row among the columns)."""
+    S, Hq, Hkv, d = 40, 4, 2, 8
+    q = _rand((S, Hq, d), 61); k = _rand((S, Hkv, d), 62)
+    v = _rand((S, Hkv, d), 63); do = _rand((S, Hq, d), 64)
+    o, lse = A.attn_fwd(q, k, v, True)
+    _, _, dk_t, dv_t = _torch_ref(q, k, v, do, True)
+    cols = np.array([0, 1, 17, S - 1])
+    dk, dv = A.attn_key_cols_given(q, do, k, v, o, lse, cols, True, row_block=16)
+    np.testing.assert_allclose(dk, dk_t[cols], rtol=0, atol=1e-10)
+    np.testing.assert_allclose(dv, dv_t[cols], rtol=0, atol=1e-10)
+
+
 ALL_PINS = [pin_brute_force, pin_torch_sdpa, pin_finite_differences,
             pin_closed_forms, pin_gradient_invariants,
-            pin_gqa_equals_repeated_mha]
+            pin_gqa_equals_repeated_mha, pin_key_cols_given_statistics]

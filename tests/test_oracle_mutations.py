@@ -40,6 +40,17 @@ MUTANTS = {
                   "dq[r, h, :] = (ds @ v[:n, g, :]) * scale"),
     "D_from_q": ("D = np.sum(do[:, h, :] * o[:, h, :], axis=1)",
                  "D = np.sum(do[:, h, :] * q[:, h, :], axis=1)"),
+    # the conditioned key columns (attn_key_cols_given)
+    "cols_drop_lse": ("np.exp(np.where(vis, s, 0.0) - lse[h, b0:b1][:, None])",
+                      "np.exp(np.where(vis, s, 0.0))"),
+    "cols_diagonal_masked": ("vis = cols[None, :] <= r[:, None] if causal",
+                             "vis = cols[None, :] < r[:, None] if causal"),
+    "cols_dv_wrong_operand": ("dv[:, g, :] += p.T @ dob[:, h, :]",
+                              "dv[:, g, :] += ds.T @ dob[:, h, :]"),
+    "cols_dk_no_scale": ("dk[:, g, :] += (ds.T @ qb[:, h, :]) / np.sqrt(d)",
+                         "dk[:, g, :] += (ds.T @ qb[:, h, :])"),
+    "cols_D_from_q": ("D = np.sum(dob[:, h, :] * ob[:, h, :], axis=1)",
+                      "D = np.sum(dob[:, h, :] * qb[:, h, :], axis=1)"),
 }
 
 
