@@ -147,7 +147,8 @@ int upipe_attn_fwd_batch(const void* q, const void* k, const void* v, void* o,
  * device array of upipe_attn_fwd_noalloc_scratch_bytes() bytes (64 MiB) that
  * each GPU the library runs on holds until the process ends.  Shapes whose
  * upipe_attn_fwd_workspace_size exceeds it return UPIPE_ERR_WORKSPACE (with
- * one key/value head and U = 1 that is S up to about 64K tokens).  The call
+ * one key/value head and U = 1: S up to 131072 when S % 128 == 0, about
+ * 65500 otherwise).  The call
  * allocates nothing; its first call on a device looks up that device's
  * copy of the array.  The stream must belong to the current device
  * (UPIPE_ERR_INVALID_ARG otherwise).  Every
