@@ -328,9 +328,11 @@ def main():
             o, lse = upipe.attn_fwd(qd, kd, vd, causal=True, U=U, ws=ws_f)
             upipe.attn_bwd(qd, kd, vd, o, lse, dod, causal=True, U=U, ws=ws_b)
 
-    for _ in range(args.warmup):
+    for i in range(args.warmup):
         step()
-    torch.cuda.synchronize()
+        torch.cuda.synchronize()
+        # progress on stderr (a long workload runs for minutes before its line)
+        print(f"bench: warmup step {i + 1}/{args.warmup} done", file=sys.stderr, flush=True)
     upipe.upipe_profile_reset()
     upipe.upipe_profile_enable(1)
     torch.cuda.synchronize()
