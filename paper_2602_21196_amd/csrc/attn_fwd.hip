@@ -169,6 +169,16 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_kernel(
 #pragma unroll
         for (int tt = 0; tt < 4; ++tt)
           st[tt] = mfma32x32x16(lds_read_b128(buf, swz256(32 * tt + r32, 2 * s + g)), qf[s], st[tt]);
+      // Keep six K fragment reads in flight ahead of the MFMAs: left alone,
+      // the scheduler reads two, waits for them and multiplies, exposing the
+      // LDS latency every two MFMAs.
+      __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
+#pragma unroll
+      for (int i = 0; i < 26; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 6, 0);
       // Mask keys past the row's last visible key (wave-uniform test first).
       if (kb + BKS - 1 > lim_w) {
 #pragma unroll
