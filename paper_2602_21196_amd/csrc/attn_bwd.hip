@@ -412,6 +412,7 @@ constexpr int DQ_T = DQ_BK * HEAD_DIM * 2;
 constexpr int DQ_OFF_K = 0, DQ_OFF_V = DQ_T;
 constexpr int DQ_STAGE = 2 * DQ_T;
 constexpr int DQ_BLK = DQ_T / 1024 / 8;   // 1 KB blocks per wave per tile
+constexpr int DQ_LA = 6;                   // K/V fragment reads kept in flight
 
 // This wave's share of one tile's copies: DQ_BLK blocks of 1 KB each of K
 // rows (transposing-read swizzle) and V rows (4 rows of 256 B per block).
@@ -496,26 +497,34 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_kernel(
     for (int h64 = 0; h64 < DQ_BK / 64; ++h64) {
       const uint32_t kb = ks + 64 * h64;
       if (CAUSAL && kb > qw + 31) break;     // rest of the tile masked for this wave
-      f32x16 sacc[2], pacc[2];
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) { sacc[hh][i] = nlse; pacc[hh][i] = 0.f; }
-#pragma unroll
-      for (int s = 0; s < 8; ++s)
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          const int row = 64 * h64 + 32 * hh + r32;
-          sacc[hh] = mfma32x32x16(lds_read_b128(buf + DQ_OFF_K, swzt(row, 2 * s + g)), qf[s], sacc[hh]);
-          pacc[hh] = mfma32x32x16(lds_read_b128(buf + DQ_OFF_V, swz256(row, 2 * s + g)), df[s], pacc[hh]);
-        }
       const bool diag = CAUSAL ? (kb + 63 > qw) : (kb + 64 > Sv);
-      bf16x8 sf[2][2];
+      // The 64 keys in two halves of 32: one score and one dP accumulator
+      // live at a time, which leaves registers for DQ_LA fragment reads in
+      // flight ahead of the S / dP MFMAs (with both halves' accumulators
+      // live the compiler kept one, waiting before every MFMA).  The dQ
+      // products still add the 16-key steps in ascending order.
 #pragma unroll
       for (int hh = 0; hh < 2; ++hh) {
+        f32x16 sacc, pacc;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) { sacc[i] = nlse; pacc[i] = 0.f; }
+#pragma unroll
+        for (int s = 0; s < 8; ++s) {
+          const int row = 64 * h64 + 32 * hh + r32;
+          sacc = mfma32x32x16(lds_read_b128(buf + DQ_OFF_K, swzt(row, 2 * s + g)), qf[s], sacc);
+          pacc = mfma32x32x16(lds_read_b128(buf + DQ_OFF_V, swz256(row, 2 * s + g)), df[s], pacc);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x100, DQ_LA, 0);
+#pragma unroll
+        for (int i = 0; i < 16 - DQ_LA; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, DQ_LA, 0);
+        bf16x8 sf[2];
         float p[16];
 #pragma unroll
-        for (int i = 0; i < 16; ++i) p[i] = fast_exp2(sacc[hh][i] * kSl2);
+        for (int i = 0; i < 16; ++i) p[i] = fast_exp2(sacc[i] * kSl2);
         if (diag) {   // wave-uniform
 #pragma unroll
           for (int i = 0; i < 16; ++i) {
@@ -525,14 +534,15 @@ __global__ __launch_bounds__(512, 1) void attn_bwd_dq_kernel(
           }
         }
 #pragma unroll
-        for (int i = 0; i < 16; ++i) sf[hh][i >> 3][i & 7] = (bf16)(p[i] * (pacc[hh][i] - Dq));
+        for (int i = 0; i < 16; ++i) sf[i >> 3][i & 7] = (bf16)(p[i] * (pacc[i] - Dq));
+#pragma unroll
+        for (int c = 0; c < 2; ++c)
+#pragma unroll
+          for (int dt = 0; dt < 4; ++dt)
+            qacc[dt] = mfma32x32x16(
+                tr_operand(buf + DQ_OFF_K, 64 * h64 + 32 * hh + 16 * c, 32 * dt, lane), sf[c],
+                qacc[dt]);
       }
-#pragma unroll
-      for (int c = 0; c < 4; ++c)
-#pragma unroll
-        for (int dt = 0; dt < 4; ++dt)
-          qacc[dt] = mfma32x32x16(tr_operand(buf + DQ_OFF_K, 64 * h64 + 16 * c, 32 * dt, lane),
-                                  sf[c >> 1][c & 1], qacc[dt]);
     }
   }
 
