@@ -215,6 +215,16 @@ __global__ __launch_bounds__(512, 1) void attn_fwd_kernel(
         for (int dt = 0; dt < 4; ++dt)
           oacc[dt] = mfma32x32x16(tr_operand(buf + K_TILE, 16 * c, 32 * dt, lane), pf[c >> 1][c & 1],
                                   oacc[dt]);
+      // Stream the V^T fragments: four (eight transposing reads) ahead, then
+      // two reads per MFMA (the default schedule issued bursts of eight
+      // reads and waited between them).
+      __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+#pragma unroll
+      for (int i = 0; i < 28; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
     }
   }
 
