@@ -3,6 +3,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <stdexcept>
+
 #include "common.h"
 
 namespace upipe {
@@ -13,7 +15,8 @@ namespace upipe {
 //   MN-major: p + (r / blk) * blk_stride + k * ld + (r % blk)
 // Rows >= rows_valid and k >= k_valid read as zero.  blk = 128 describes the
 // head-major chunk buffers [U][Sp][128]; an unblocked operand uses a block
-// larger than any index and blk_stride = 0.
+// larger than any index and blk_stride = 0.  blk must be a power of two (the
+// kernel splits an index with a shift and a mask).
 struct GemmOperand {
   const bf16* p;
   int64_t ld;
@@ -27,6 +30,8 @@ constexpr int64_t kNoBlock = int64_t(1) << 50;
 
 inline GemmOperand operand(const bf16* p, int64_t ld, int64_t rows_valid, int64_t k_valid,
                            int64_t blk = kNoBlock, int64_t blk_stride = 0) {
+  static_assert((kNoBlock & (kNoBlock - 1)) == 0, "kNoBlock must be a power of two");
+  if (blk <= 0 || (blk & (blk - 1)) != 0) throw std::invalid_argument("GEMM block width");
   return GemmOperand{p, ld, blk, blk_stride, rows_valid, k_valid};
 }
 

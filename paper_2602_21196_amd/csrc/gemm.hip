@@ -33,10 +33,14 @@ constexpr int BM = 128, BN = 128, BKG = 128;
 constexpr int TILE_BYTES = 128 * 256;     // 32 KB per operand per stage
 
 // Address of operand element (r, k).
+// The block width is a power of two (128, or the unblocked 2^50), so the
+// block index and the offset inside it are a shift and a mask.
 __device__ __forceinline__ const bf16* elem_ptr(const GemmOperand& o, bool kmajor, int64_t r,
                                                 int64_t k) {
-  if (kmajor) return o.p + (k / o.blk) * o.blk_stride + r * o.ld + (k % o.blk);
-  return o.p + (r / o.blk) * o.blk_stride + k * o.ld + (r % o.blk);
+  const int sh = __builtin_ctzll((unsigned long long)o.blk);
+  const int64_t mask = o.blk - 1;
+  if (kmajor) return o.p + (k >> sh) * o.blk_stride + r * o.ld + (k & mask);
+  return o.p + (r >> sh) * o.blk_stride + k * o.ld + (r & mask);
 }
 
 // Buffer resource over the operand's tile at (r0, k0), bounded by the valid
